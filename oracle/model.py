@@ -1,0 +1,164 @@
+"""Qwen2.5 decoder forward in fp64 -- oracle, test infrastructure only.
+
+The paper runs rollout with Qwen2.5 models (section 6, "Models") but writes no
+model equations; this module is the standard Qwen2.5 decoder written out
+directly from its definition:
+
+  x_i = E[t_i]
+  per layer:  h = RMSNorm(x) ; q,k,v = W h + b ; RoPE(q, k) at position i ;
+              causal GQA softmax attention ; x += W_o a ;
+              h2 = RMSNorm(x) ; x += W_down (silu(W_gate h2) * (W_up h2))
+  logits = W_lm RMSNorm(x)   (W_lm = E when embeddings are tied)
+
+Weights are given in [out, in] layout, so a projection is ``h @ W.T``.
+RoPE pairs dimension d with d + hd/2 ("rotate half"), with frequencies
+theta^(-2d/hd) and angles computed in fp64.  Query head h reads KV head
+h // (n_q / n_kv).  No padding: positions are 0-based and contiguous.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * g over the last axis."""
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * g
+
+
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def rope_cos_sin(positions: np.ndarray, head_dim: int, theta: float):
+    """cos/sin of angle pos * theta^(-2d/hd), d < hd/2, in fp64. Shapes [n, hd/2]."""
+    d = np.arange(head_dim // 2, dtype=np.float64)
+    inv_freq = theta ** (-2.0 * d / head_dim)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * inv_freq[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def apply_rope(u: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    """Rotate pairs (d, d + hd/2) of u [n, heads, hd] by the per-row angles."""
+    half = u.shape[-1] // 2
+    u1, u2 = u[..., :half], u[..., half:]
+    c, s = cos[:, None, :], sin[:, None, :]
+    return np.concatenate([u1 * c - u2 * s, u2 * c + u1 * s], axis=-1)
+
+
+def softmax(s: np.ndarray, axis: int = -1) -> np.ndarray:
+    m = np.max(s, axis=axis, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=axis, keepdims=True)
+
+
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos: np.ndarray,
+              k_pos: np.ndarray) -> np.ndarray:
+    """Causal GQA attention.
+
+    q [nq_tok, n_q, hd], k/v [nk_tok, n_kv, hd]; query at position q_pos[i]
+    attends to keys with k_pos <= q_pos[i].  Returns [nq_tok, n_q, hd].
+    """
+    n_q, n_kv, hd = q.shape[1], k.shape[1], q.shape[2]
+    group = n_q // n_kv
+    out = np.empty_like(q)
+    mask = k_pos[None, :] <= q_pos[:, None]                    # [nq_tok, nk_tok]
+    for h in range(n_q):
+        kh = h // group
+        s = q[:, h, :] @ k[:, kh, :].T / np.sqrt(hd)           # [nq_tok, nk_tok]
+        s = np.where(mask, s, -np.inf)
+        out[:, h, :] = softmax(s, axis=-1) @ v[:, kh, :]
+    return out
+
+
+def _qkv(layer, h, shape):
+    hd = shape.head_dim
+    q = (h @ layer["wq"].T + layer["bq"]).reshape(-1, shape.n_q, hd)
+    k = (h @ layer["wk"].T + layer["bk"]).reshape(-1, shape.n_kv, hd)
+    v = (h @ layer["wv"].T + layer["bv"]).reshape(-1, shape.n_kv, hd)
+    return q, k, v
+
+
+def _mlp(layer, x, shape):
+    h2 = rmsnorm(x, layer["mlp_norm"], shape.eps)
+    return (silu(h2 @ layer["w_gate"].T) * (h2 @ layer["w_up"].T)) @ layer["w_down"].T
+
+
+def lm_head(w, x, shape) -> np.ndarray:
+    hf = rmsnorm(x, w["final_norm"], shape.eps)
+    wl = w["embed"] if w["lm_head"] is None else w["lm_head"]
+    return hf @ wl.T
+
+
+def forward_full(w: dict, shape, tokens) -> np.ndarray:
+    """Brute-force causal forward over a whole sequence: logits [n, V] for every position."""
+    tokens = np.asarray(tokens)
+    n = len(tokens)
+    pos = np.arange(n)
+    cos, sin = rope_cos_sin(pos, shape.head_dim, shape.theta)
+    x = w["embed"][tokens].astype(np.float64)
+    for layer in w["layers"]:
+        h = rmsnorm(x, layer["attn_norm"], shape.eps)
+        q, k, v = _qkv(layer, h, shape)
+        q, k = apply_rope(q, cos, sin), apply_rope(k, cos, sin)
+        a = attention(q, k, v, pos, pos).reshape(n, -1)
+        x = x + a @ layer["wo"].T
+        x = x + _mlp(layer, x, shape)
+    return lm_head(w, x, shape)
+
+
+class KVState:
+    """Incremental decoding state of one sequence: post-RoPE K and V per layer."""
+
+    def __init__(self, shape):
+        self.shape = shape
+        self.k = [np.zeros((0, shape.n_kv, shape.head_dim)) for _ in range(shape.layers)]
+        self.v = [np.zeros((0, shape.n_kv, shape.head_dim)) for _ in range(shape.layers)]
+        self.length = 0
+
+    def step(self, w: dict, tokens) -> np.ndarray:
+        """Append tokens at positions length.. and return their logits [n, V]."""
+        shape = self.shape
+        tokens = np.asarray(tokens)
+        n = len(tokens)
+        pos = np.arange(self.length, self.length + n)
+        cos, sin = rope_cos_sin(pos, shape.head_dim, shape.theta)
+        x = w["embed"][tokens].astype(np.float64)
+        for li, layer in enumerate(w["layers"]):
+            h = rmsnorm(x, layer["attn_norm"], shape.eps)
+            q, k, v = _qkv(layer, h, shape)
+            q, k = apply_rope(q, cos, sin), apply_rope(k, cos, sin)
+            self.k[li] = np.concatenate([self.k[li], k])
+            self.v[li] = np.concatenate([self.v[li], v])
+            kpos = np.arange(self.length + n)
+            a = attention(q, self.k[li], self.v[li], pos, kpos).reshape(n, -1)
+            x = x + a @ layer["wo"].T
+            x = x + _mlp(layer, x, shape)
+        self.length += n
+        return lm_head(w, x, shape)
+
+
+def generate(w: dict, shape, prompt, n_new: int, sample_fn) -> tuple:
+    """Rollout of one sequence: prefill the prompt, then n_new - 1 decode steps.
+
+    ``n_new`` counts every generated token, the one sampled from the prefill
+    logits included; the KV of the last generated token is never needed.
+    ``sample_fn(logits_row, pos)`` returns the token at absolute position pos.
+    Returns (tokens [n_new], logits [n_new, V]) where logits[j] produced tokens[j].
+    """
+    st = KVState(shape)
+    logits = st.step(w, prompt)[-1]
+    p = len(prompt)
+    toks, rows = [], []
+    for j in range(n_new):
+        t = int(sample_fn(logits, p + j))
+        toks.append(t)
+        rows.append(logits)
+        if j + 1 < n_new:
+            logits = st.step(w, [t])[-1]
+    return np.array(toks, np.int32), np.array(rows)
+
+
+def teacher_forced_logits(w: dict, shape, prompt, response) -> np.ndarray:
+    """Logits that predict response[j] given prompt + response[:j], rows j = 0..L-1."""
+    seq = np.concatenate([np.asarray(prompt), np.asarray(response)[:-1]])
+    return forward_full(w, shape, seq)[len(prompt) - 1:]
