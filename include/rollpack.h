@@ -1,0 +1,246 @@
+/*
+ * rollpack.h -- C ABI of the MI355X rollout library.
+ *
+ * Rollout is the generation stage of synchronous RL post-training (paper
+ * section 2.1): the actor model receives P0 prompts and produces R0
+ * responses for each, and the stage must finish before training starts.
+ * Response lengths are long-tailed (section 2.2), so a batch shrinks as short
+ * responses finish while the longest keep the GPU busy; tail batching
+ * (section 3) groups prompts into balanced short rounds and consolidated long
+ * rounds.  This library generates responses for a batch of sequences with a
+ * Qwen2.5-style decoder on one gfx950 GPU and plans tail-batched rounds.
+ *
+ * Conventions for every call:
+ *  - Device pointers are HIP device addresses; host pointers are ordinary
+ *    process memory.  Each argument says which it is.
+ *  - The caller owns every buffer (weights, KV pool, scratch workspace,
+ *    outputs).  Device buffers passed to rp_engine_create must stay valid
+ *    until rp_engine_destroy.  Host arrays are read only during the call.
+ *    The engine never allocates device memory.
+ *  - Every call returns rp_status.  On failure a message is available from
+ *    rp_last_error() (thread-local) and the engine state is unchanged,
+ *    except after RP_ERR_HIP, which leaves the engine unusable.
+ *  - All device work is ordered on the stream given at creation.  A call
+ *    returns once its host-visible outputs are ready; device outputs are
+ *    ready in stream order.  An engine is not thread-safe.
+ *  - Sequences are identified by caller-chosen 64-bit ids, unique among the
+ *    engine's live sequences.  The id keys the sampling noise, so a
+ *    sequence's tokens do not depend on batching or scheduling.
+ */
+#ifndef ROLLPACK_H
+#define ROLLPACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rp_status {
+  RP_OK = 0,
+  RP_ERR_INVALID_ARG = 1,   /* a size, pointer or value is out of range */
+  RP_ERR_OUT_OF_PAGES = 2,  /* the KV pool cannot hold the admitted sequences */
+  RP_ERR_DUPLICATE_ID = 3,  /* a sequence id is already live */
+  RP_ERR_UNKNOWN_ID = 4,    /* a sequence id is not live */
+  RP_ERR_BAD_STATE = 5,     /* the call does not fit the engine's state */
+  RP_ERR_HIP = 6,           /* a HIP runtime call failed */
+  RP_ERR_CAPACITY = 7       /* more sequences, tokens or context than the limits allow */
+} rp_status;
+
+typedef enum rp_dtype {
+  RP_DTYPE_F32 = 0,   /* weights, GEMM inputs and KV in fp32 */
+  RP_DTYPE_BF16 = 1   /* weights, GEMM inputs and KV in bf16; fp32 accumulation,
+                         residual stream, norms, softmax and logits */
+} rp_dtype;
+
+/* Qwen2.5 decoder shape (the paper's models, section 6).  q/k/v carry a
+ * bias, o/gate/up/down do not; RMSNorm with eps; rotate-half RoPE with base
+ * rope_theta; query head h reads KV head h / (n_q_heads / n_kv_heads). */
+typedef struct rp_model_config {
+  int32_t n_layers;
+  int32_t hidden;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;          /* 64 or 128 */
+  int32_t intermediate;
+  int32_t vocab;
+  float rms_eps;
+  float rope_theta;
+  int32_t tied_embeddings;   /* 1: the LM head is the embedding matrix */
+  int32_t dtype;             /* rp_dtype */
+} rp_model_config;
+
+/* Device pointers to one layer's tensors, element type = config dtype,
+ * [out, in] row-major: wq [n_q*hd, H], wk/wv [n_kv*hd, H], wo [H, n_q*hd],
+ * w_gate/w_up [I, H], w_down [H, I]; bq [n_q*hd], bk/bv [n_kv*hd];
+ * attn_norm/mlp_norm [H]. */
+typedef struct rp_layer_weights {
+  const void* attn_norm;
+  const void* wq;
+  const void* bq;
+  const void* wk;
+  const void* bk;
+  const void* wv;
+  const void* bv;
+  const void* wo;
+  const void* mlp_norm;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+} rp_layer_weights;
+
+typedef struct rp_weights {
+  const void* embed;                /* device [V, H] */
+  const void* final_norm;           /* device [H] */
+  const void* lm_head;              /* device [V, H]; NULL when tied */
+  const rp_layer_weights* layers;   /* HOST array [n_layers], copied at create */
+} rp_weights;
+
+typedef struct rp_engine_limits {
+  int32_t max_seqs;            /* sequences live at once (KV slots), >= 1 */
+  int32_t max_prefill_tokens;  /* prompt tokens per prefill chunk, >= longest prompt */
+  int32_t max_context;         /* longest prompt + response, <= 65536 */
+  int32_t page_tokens;         /* tokens per KV page; must be 64 */
+  int64_t kv_pages;            /* pages in the KV pool */
+} rp_engine_limits;
+
+typedef struct rp_engine rp_engine;
+
+/* Per-round measurements of rp_rollout_generate.  Times come from HIP events
+ * on the engine's stream.  slot_idle is the fraction of sequence-slot time
+ * spent after a sequence finished while its round was still running: the
+ * bubble of section 2.2 counted per sequence slot. */
+typedef struct rp_round_stats {
+  int32_t round_id;
+  int32_t n_seqs;
+  int32_t decode_steps;
+  int32_t reserved;
+  int64_t prompt_tokens;
+  int64_t generated_tokens;
+  int64_t peak_pages;
+  double makespan_ms;      /* first prefill kernel to the last token of the round */
+  double prefill_ms;
+  double decode_ms;
+  double slot_idle;        /* in [0, 1] */
+  double idle_slot_s;      /* sum over sequences of (round end - own finish), seconds */
+} rp_round_stats;
+
+/* Bytes of the caller-provided KV pool and scratch workspace for this model
+ * and these limits.  kv_bytes covers limits->kv_pages pages; both are
+ * multiples of 256. */
+rp_status rp_workspace_size(const rp_model_config* cfg, const rp_engine_limits* limits,
+                            size_t* kv_bytes, size_t* scratch_bytes);
+
+/* Bytes of KV cache one token occupies (all layers, K and V). */
+rp_status rp_kv_bytes_per_token(const rp_model_config* cfg, size_t* bytes);
+
+/* Create an engine over caller-owned device memory.  kv_ws/scratch_ws must
+ * be at least the sizes rp_workspace_size returns and 256-byte aligned;
+ * hip_stream is a hipStream_t (NULL = default stream).  The weights are not
+ * copied; their device memory must outlive the engine. */
+rp_status rp_engine_create(const rp_model_config* cfg, const rp_weights* weights,
+                           const rp_engine_limits* limits, void* kv_ws, size_t kv_bytes,
+                           void* scratch_ws, size_t scratch_bytes, void* hip_stream,
+                           rp_engine** out);
+
+void rp_engine_destroy(rp_engine* eng);
+
+/* Admit n sequences and run their prompts through the model (prefill), then
+ * sample each sequence's first response token.
+ *   seq_ids         host [n], new unique ids
+ *   prompt_tokens   host, all prompts concatenated (CSR), ids in [0, V)
+ *   prompt_offsets  host [n+1], prompt i is tokens [off[i], off[i+1]), length >= 1
+ *   max_new_tokens  host [n], >= 1: every generated token counts, the one
+ *                   sampled here included; generation stops there (forced
+ *                   lengths, no end-of-sequence token)
+ *   seed, temperature: the sampling key and temperature of these sequences;
+ *                   temperature 0 is greedy
+ *   logits_out      DEVICE [n, V] fp32 or NULL: logits of each prompt's last position
+ *   first_tokens_out HOST [n] or NULL: the sampled first tokens (synchronises)
+ * KV pages for prompt + max_new_tokens - 1 positions are reserved at
+ * admission; RP_ERR_OUT_OF_PAGES if the pool cannot hold them. */
+rp_status rp_prefill(rp_engine* eng, int32_t n, const int64_t* seq_ids,
+                     const int32_t* prompt_tokens, const int64_t* prompt_offsets,
+                     const int32_t* max_new_tokens, uint64_t seed, float temperature,
+                     float* logits_out, int32_t* first_tokens_out);
+
+/* One decode step for every live, unfinished sequence ("row"), rows in
+ * admission order.  Each row feeds its last sampled token (or
+ * forced_tokens[row], teacher forcing: the input changes, the sampled history
+ * does not), appends its K/V, and samples its next token.
+ *   forced_tokens   HOST [n_active] or NULL
+ *   logits_out      DEVICE [n_active, V] fp32 or NULL
+ *   row_ids_out     HOST [max_seqs] or NULL: the sequence id of each row
+ *   n_active_out    HOST, the number of rows in this step (0: nothing to do)
+ * A sequence that reaches its max_new_tokens becomes finished and keeps its
+ * pages until rp_free_finished. */
+rp_status rp_decode_step(rp_engine* eng, const int32_t* forced_tokens, float* logits_out,
+                         int64_t* row_ids_out, int32_t* n_active_out);
+
+/* Release the KV pages and slots of finished sequences and report their ids
+ * (host [cap]).  The tokens of a released sequence are no longer available. */
+rp_status rp_free_finished(rp_engine* eng, int64_t* finished_ids_out, int32_t cap,
+                           int32_t* n_finished_out);
+
+/* Stop live sequences now (speculative abort, section 3) and release them. */
+rp_status rp_abort(rp_engine* eng, int32_t n, const int64_t* seq_ids);
+
+/* Copy the generated tokens of a live sequence to host out [cap]; len_out
+ * gets the number generated so far.  Synchronises the stream. */
+rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t cap,
+                        int32_t* len_out);
+
+/* Whole-batch rollout: generate max_new_tokens[i] tokens for each of n
+ * sequences, round by round (rounds in increasing round_ids order; NULL =
+ * one round).  Within a round all sequences are admitted together (prefill
+ * in chunks), then decoded until the last one finishes, freeing KV pages as
+ * sequences finish so the batch shrinks.
+ *   seq_ids, prompt_tokens, prompt_offsets, max_new_tokens: as rp_prefill
+ *   round_ids       host [n] or NULL
+ *   resp_tokens_out host [sum max_new_tokens]: sequence i's tokens at
+ *                   offset sum_{j<i} max_new_tokens[j]
+ *   stats_out       host [max_stats] or NULL: one record per round, in order
+ *   n_rounds_out    host or NULL
+ * The engine must have no live sequences. */
+rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
+                              const int32_t* prompt_tokens, const int64_t* prompt_offsets,
+                              const int32_t* max_new_tokens, uint64_t seed, float temperature,
+                              const int32_t* round_ids, int32_t* resp_tokens_out,
+                              rp_round_stats* stats_out, int32_t max_stats,
+                              int32_t* n_rounds_out);
+
+/* Tail-batching plan (section 3), host only.  n_prompts prompts, submitted
+ * in order, each with r_spec = ceil(eta * R0) candidate responses of known
+ * lengths lens[p * r_spec + r] (decode steps).  A short round launches the
+ * next ceil(eta * P0) fresh prompts and keeps the first P0 to have R0
+ * finished responses (ties: lower index), each with its R0 shortest
+ * responses; the round ends when its P0-th prompt completes and the other
+ * prompts join a FIFO long-prompt queue.  When the queue holds P0 prompts,
+ * or no fresh prompt is left, a long round runs up to P0 queued prompts with
+ * R0 responses each and no speculation.
+ *   round_kind_out  host [max_rounds]: 0 short, 1 long
+ *   round_time_out  host [max_rounds]: round length in decode steps
+ *   launch_off_out  host [max_rounds + 1]: CSR offsets into launch_prompt_out
+ *   launch_prompt_out host [cap_launch]: prompts launched per round, ascending
+ *   run_steps_out   host [cap_launch * r_spec]: steps each launched response ran
+ *                   (responses r >= R0 of a long round run 0 steps)
+ *   accept_round_out host [n_prompts]: round that accepted each prompt
+ *   kept_out        host [n_prompts * r_spec]: 1 if the response is kept
+ *   n_rounds_out    host */
+rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens,
+                                int32_t P0, int32_t R0, float eta, int32_t max_rounds,
+                                int32_t cap_launch, int32_t* round_kind_out,
+                                int32_t* round_time_out, int32_t* launch_off_out,
+                                int32_t* launch_prompt_out, int32_t* run_steps_out,
+                                int32_t* accept_round_out, int32_t* kept_out,
+                                int32_t* n_rounds_out);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* rp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROLLPACK_H */

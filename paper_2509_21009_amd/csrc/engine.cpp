@@ -1,0 +1,725 @@
+// Rollout engine: admission with paged KV reservation, chunked prefill, the
+// decode step loop and round-by-round rollout with per-round measurements.
+//
+// Rollout (paper section 2.1) generates R0 responses for each of P0 prompts;
+// the batch shrinks as responses finish (section 2.2), so finished
+// sequences give their KV pages back and later steps run with fewer rows.
+// All device work is enqueued on one stream; per-step metadata is O(rows)
+// integers copied from pinned staging buffers.
+#include "engine.hpp"
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <numeric>
+
+namespace rollpack {
+
+namespace {
+
+constexpr int kMaxGemmSplits = 8;
+
+void hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess) throw RpError(RP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+#define HIP_TRY(expr) hip_check((expr), #expr)
+
+size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+int decode_split_target(const rp_model_config& c) { return std::max(1, 2048 / c.n_kv_heads); }
+
+}  // namespace
+
+void validate_config(const rp_model_config& c) {
+  auto bad = [](const std::string& m) { throw RpError(RP_ERR_INVALID_ARG, m); };
+  if (c.n_layers < 1 || c.hidden < 1 || c.n_q_heads < 1 || c.n_kv_heads < 1 || c.intermediate < 1 ||
+      c.vocab < 2)
+    bad("model config: sizes must be positive");
+  if (c.n_q_heads % c.n_kv_heads != 0) bad("model config: n_q_heads must be a multiple of n_kv_heads");
+  if (c.head_dim != 64 && c.head_dim != 128) bad("model config: head_dim must be 64 or 128");
+  if (c.dtype != RP_DTYPE_F32 && c.dtype != RP_DTYPE_BF16) bad("model config: unknown dtype");
+  if (!(c.rms_eps > 0.f) || !(c.rope_theta > 1.f)) bad("model config: rms_eps > 0 and rope_theta > 1 required");
+  if (c.dtype == RP_DTYPE_BF16) {
+    const int nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+    if (c.n_q_heads / c.n_kv_heads > 16) bad("bf16 path: at most 16 query heads per KV head");
+    if (c.hidden % 128 || c.intermediate % 128 || (c.n_q_heads * c.head_dim) % 128 || nqkv % 128 ||
+        c.vocab % 128)
+      bad("bf16 path: hidden, intermediate, n_q*head_dim, qkv width and vocab must be multiples of 128");
+  }
+}
+
+void validate_limits(const rp_engine_limits& l) {
+  if (l.page_tokens != kPageTokens) throw RpError(RP_ERR_INVALID_ARG, "limits: page_tokens must be 64");
+  if (l.max_seqs < 1 || l.max_prefill_tokens < 1 || l.max_context < 2 || l.max_context > 65536 ||
+      l.kv_pages < 1 || l.kv_pages > (int64_t{1} << 24) || l.max_seqs > (1 << 20) || l.max_prefill_tokens > (1 << 22))
+    throw RpError(RP_ERR_INVALID_ARG,
+                  "limits: 1 <= max_seqs <= 2^20, 1 <= max_prefill_tokens <= 2^22, 1 <= kv_pages <= 2^24, "
+                  "2 <= max_context <= 65536");
+}
+
+size_t kv_pool_bytes(const rp_model_config& c, int64_t pages) {
+  const size_t esz = c.dtype == RP_DTYPE_BF16 ? 2 : 4;
+  return align256(static_cast<size_t>(pages) * c.n_layers * 2 * c.n_kv_heads * kPageTokens * c.head_dim * esz);
+}
+
+ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l) {
+  ScratchPlan p{};
+  const size_t esz = c.dtype == RP_DTYPE_BF16 ? 2 : 4;
+  const size_t H = c.hidden, I = c.intermediate, V = c.vocab, hd = c.head_dim;
+  const size_t nq = c.n_q_heads, nkv = c.n_kv_heads;
+  const size_t nqkv = (nq + 2 * nkv) * hd;
+  const size_t mmax = std::max<size_t>(l.max_prefill_tokens, l.max_seqs);
+  const size_t nmax = std::max(nqkv, H);
+  p.max_pages = static_cast<int32_t>((l.max_context + kPageTokens - 1) / kPageTokens);
+  p.split_cap = c.dtype == RP_DTYPE_BF16 ? decode_split_target(c) + l.max_seqs : 0;
+  p.part_elems = std::max(static_cast<size_t>(l.max_prefill_tokens) * nmax,
+                          static_cast<size_t>(kMaxGemmSplits) * l.max_seqs * nmax);
+  const size_t T = l.max_prefill_tokens, S = l.max_seqs;
+  p.meta_ints = static_cast<int32_t>(std::max(7 * S + 1, 3 * T + 8 * S + 1));
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  p.x = take(mmax * H * 4);
+  p.h = take(mmax * H * esz);
+  p.part = take(p.part_elems * 4);
+  p.q = take(mmax * nq * hd * esz);
+  p.attn = take(mmax * nq * hd * esz);
+  p.act = take(mmax * I * esz);
+  p.hsel = take(S * H * esz);
+  p.logits = take(S * V * 4);
+  p.att_o = take(static_cast<size_t>(p.split_cap) * nkv * 16 * hd * 4);
+  p.att_ml = take(static_cast<size_t>(p.split_cap) * nkv * 32 * 4);
+  p.rope_cos = take(static_cast<size_t>(l.max_context) * (hd / 2) * 4);
+  p.rope_sin = take(static_cast<size_t>(l.max_context) * (hd / 2) * 4);
+  p.page_table = take(S * p.max_pages * 4);
+  p.tokens_cur = take(S * 4);
+  p.hist = take(S * static_cast<size_t>(l.max_context) * 4);
+  p.resp = take(S * static_cast<size_t>(l.max_context) * 4);
+  p.slot_seed = take(S * 8);
+  p.slot_id = take(S * 8);
+  p.slot_temp = take(S * 4);
+  p.meta = take(static_cast<size_t>(p.meta_ints) * 4);
+  p.total = off;
+  return p;
+}
+
+Engine::Engine(const rp_model_config& cfg, const rp_weights& w, const rp_engine_limits& lim, void* kv_ws,
+               size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, hipStream_t stream)
+    : cfg_(cfg), lim_(lim), stream_(stream), pool_(lim.kv_pages) {
+  validate_config(cfg);
+  validate_limits(lim);
+  bf16_ = cfg.dtype == RP_DTYPE_BF16;
+  esz_ = bf16_ ? 2 : 4;
+  nqkv_ = (cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
+  plan_ = plan_scratch(cfg, lim);
+  if (!kv_ws || !scratch_ws || (reinterpret_cast<uintptr_t>(kv_ws) & 255) ||
+      (reinterpret_cast<uintptr_t>(scratch_ws) & 255))
+    throw RpError(RP_ERR_INVALID_ARG, "workspaces must be non-null and 256-byte aligned");
+  if (kv_bytes < kv_pool_bytes(cfg, lim.kv_pages) || scratch_bytes < plan_.total)
+    throw RpError(RP_ERR_INVALID_ARG, "workspace smaller than rp_workspace_size");
+  if (!w.embed || !w.final_norm || !w.layers || (!cfg.tied_embeddings && !w.lm_head))
+    throw RpError(RP_ERR_INVALID_ARG, "weights: embed, final_norm, layers (and lm_head unless tied) required");
+  layers_.assign(w.layers, w.layers + cfg.n_layers);
+  for (const auto& L : layers_) {
+    if (!L.attn_norm || !L.wq || !L.bq || !L.wk || !L.bk || !L.wv || !L.bv || !L.wo || !L.mlp_norm ||
+        !L.w_gate || !L.w_up || !L.w_down)
+      throw RpError(RP_ERR_INVALID_ARG, "weights: a layer tensor pointer is null");
+  }
+  w_ = w;
+  w_.layers = layers_.data();
+  if (cfg.tied_embeddings) w_.lm_head = w.embed;
+  kv_ = static_cast<char*>(kv_ws);
+  scratch_ = static_cast<char*>(scratch_ws);
+  layer_kv_bytes_ = static_cast<size_t>(lim.kv_pages) * cfg.n_kv_heads * kPageTokens * cfg.head_dim * esz_;
+
+  slots_.resize(lim.max_seqs);
+  for (int32_t s = lim.max_seqs - 1; s >= 0; --s) free_slots_.push_back(s);
+
+  const size_t pt_bytes = static_cast<size_t>(lim.max_seqs) * plan_.max_pages * 4;
+  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_page_table_), pt_bytes, hipHostMallocDefault));
+  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_slot_seed_), lim.max_seqs * 8, hipHostMallocDefault));
+  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_slot_id_), lim.max_seqs * 8, hipHostMallocDefault));
+  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_slot_temp_), lim.max_seqs * 4, hipHostMallocDefault));
+  std::memset(h_page_table_, 0, pt_bytes);
+  std::memset(h_slot_seed_, 0, lim.max_seqs * 8);
+  std::memset(h_slot_id_, 0, lim.max_seqs * 8);
+  std::memset(h_slot_temp_, 0, lim.max_seqs * 4);
+  HIP_TRY(hipEventCreateWithFlags(&ev_tables_, hipEventDisableTiming));
+  ring_bytes_ = static_cast<size_t>(plan_.meta_ints) * 4;
+  ring_.resize(8);
+  for (auto& r : ring_) {
+    HIP_TRY(hipHostMalloc(&r.host, ring_bytes_, hipHostMallocDefault));
+    HIP_TRY(hipEventCreateWithFlags(&r.ev, hipEventDisableTiming));
+  }
+
+  // RoPE table: angle = pos * theta^(-2d/hd), computed in double, stored fp32.
+  const int half = cfg.head_dim / 2;
+  std::vector<float> cs(static_cast<size_t>(lim.max_context) * half), sn(cs.size());
+  for (int pos = 0; pos < lim.max_context; ++pos)
+    for (int d = 0; d < half; ++d) {
+      const double inv = std::pow(static_cast<double>(cfg.rope_theta), -2.0 * d / cfg.head_dim);
+      const double ang = static_cast<double>(pos) * inv;
+      cs[static_cast<size_t>(pos) * half + d] = static_cast<float>(std::cos(ang));
+      sn[static_cast<size_t>(pos) * half + d] = static_cast<float>(std::sin(ang));
+    }
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, stream_));
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, stream_));
+  // Zero the KV pool once: masked-out tail tokens of a page are multiplied by
+  // zero probabilities, which must not meet NaN bit patterns.
+  HIP_TRY(hipMemsetAsync(kv_, 0, kv_pool_bytes(cfg, lim.kv_pages), stream_));
+  HIP_TRY(hipMemsetAsync(scratch_ + plan_.page_table, 0, pt_bytes, stream_));
+  HIP_TRY(hipMemsetAsync(scratch_ + plan_.tokens_cur, 0, lim.max_seqs * 4, stream_));
+  HIP_TRY(hipStreamSynchronize(stream_));
+}
+
+Engine::~Engine() {
+  (void)hipStreamSynchronize(stream_);
+  for (auto& r : ring_) {
+    if (r.host) (void)hipHostFree(r.host);
+    if (r.ev) (void)hipEventDestroy(r.ev);
+  }
+  for (auto e : events_) (void)hipEventDestroy(e);
+  if (ev_tables_) (void)hipEventDestroy(ev_tables_);
+  if (h_page_table_) (void)hipHostFree(h_page_table_);
+  if (h_slot_seed_) (void)hipHostFree(h_slot_seed_);
+  if (h_slot_id_) (void)hipHostFree(h_slot_id_);
+  if (h_slot_temp_) (void)hipHostFree(h_slot_temp_);
+}
+
+int32_t* Engine::stage_meta(size_t ints) {
+  if (ints * 4 > ring_bytes_) throw RpError(RP_ERR_CAPACITY, "step metadata exceeds the staging capacity");
+  Staging& st = ring_[ring_next_];
+  if (st.pending) {
+    HIP_TRY(hipEventSynchronize(st.ev));
+    st.pending = false;
+  }
+  return static_cast<int32_t*>(st.host);
+}
+
+void Engine::upload_meta(const int32_t* host, size_t ints) {
+  Staging& st = ring_[ring_next_];
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.meta, host, ints * 4, hipMemcpyHostToDevice, stream_));
+  HIP_TRY(hipEventRecord(st.ev, stream_));
+  st.pending = true;
+  ring_next_ = (ring_next_ + 1) % ring_.size();
+  d_meta_ = sp<int32_t>(plan_.meta);
+}
+
+void Engine::upload_slot_tables() {
+  const size_t pt_bytes = static_cast<size_t>(lim_.max_seqs) * plan_.max_pages * 4;
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.page_table, h_page_table_, pt_bytes, hipMemcpyHostToDevice, stream_));
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.slot_seed, h_slot_seed_, lim_.max_seqs * 8, hipMemcpyHostToDevice, stream_));
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.slot_id, h_slot_id_, lim_.max_seqs * 8, hipMemcpyHostToDevice, stream_));
+  HIP_TRY(hipMemcpyAsync(scratch_ + plan_.slot_temp, h_slot_temp_, lim_.max_seqs * 4, hipMemcpyHostToDevice, stream_));
+  HIP_TRY(hipEventRecord(ev_tables_, stream_));
+  tables_pending_ = true;
+}
+
+void Engine::check_admission(int32_t n, const int64_t* ids, const int64_t* offs, const int32_t* toks,
+                             const int32_t* max_new, float temp) const {
+  if (n < 1 || !ids || !offs || !toks || !max_new) throw RpError(RP_ERR_INVALID_ARG, "prefill: null array or n < 1");
+  if (!(temp >= 0.f) || std::isinf(temp)) throw RpError(RP_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+  if (offs[0] != 0) throw RpError(RP_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
+  if (n > static_cast<int32_t>(free_slots_.size()))
+    throw RpError(RP_ERR_CAPACITY, "more sequences than free slots (max_seqs)");
+  std::unordered_map<int64_t, int> seen;
+  int64_t pages = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const int64_t p = offs[i + 1] - offs[i];
+    if (p < 1) throw RpError(RP_ERR_INVALID_ARG, "every prompt needs at least one token");
+    if (p > lim_.max_prefill_tokens) throw RpError(RP_ERR_CAPACITY, "prompt longer than max_prefill_tokens");
+    if (max_new[i] < 1) throw RpError(RP_ERR_INVALID_ARG, "max_new_tokens must be >= 1");
+    if (p + max_new[i] - 1 > lim_.max_context) throw RpError(RP_ERR_CAPACITY, "prompt + max_new_tokens - 1 exceeds max_context");
+    if (id2slot_.count(ids[i]) || seen.count(ids[i])) throw RpError(RP_ERR_DUPLICATE_ID, "sequence id already live");
+    seen[ids[i]] = 1;
+    for (int64_t t = offs[i]; t < offs[i + 1]; ++t)
+      if (toks[t] < 0 || toks[t] >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "prompt token id out of range");
+    pages += PagePool::pages_for(p + max_new[i] - 1, kPageTokens);
+  }
+  if (!pool_.can_take(pages)) throw RpError(RP_ERR_OUT_OF_PAGES, "KV pool cannot hold the admitted sequences");
+}
+
+void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_splits, int tps) {
+  const int H = cfg_.hidden, I = cfg_.intermediate, V = cfg_.vocab, hd = cfg_.head_dim;
+  const int nq = cfg_.n_q_heads, nkv = cfg_.n_kv_heads;
+  const float eps = cfg_.rms_eps;
+  hipStream_t s = stream_;
+  float* x = sp<float>(plan_.x);
+  void* h = scratch_ + plan_.h;
+  float* part = sp<float>(plan_.part);
+  void* q = scratch_ + plan_.q;
+  void* attn = scratch_ + plan_.attn;
+  void* act = scratch_ + plan_.act;
+  int32_t* tokens_cur = sp<int32_t>(plan_.tokens_cur);
+  const int32_t* pt = sp<int32_t>(plan_.page_table);
+
+  auto splits_for = [&](int N, int K) {
+    int sp_ = gemm_pick_splits(bf16_, M, N, K, kMaxGemmSplits);
+    const size_t cap = plan_.part_elems / (static_cast<size_t>(M) * N);
+    if (static_cast<size_t>(sp_) > cap) sp_ = static_cast<int>(std::max<size_t>(cap, 1));
+    return sp_;
+  };
+
+  EmbedArgs ea{w_.embed, layers_[0].attn_norm, m_in_tok_, m_slot_, tokens_cur, M, H, eps, x, h};
+  HIP_TRY(launch_embed_norm(bf16_, ea, s));
+
+  const int s_qkv = splits_for(nqkv_, H);
+  const int s_o = splits_for(H, nq * hd);
+  const int s_d = splits_for(H, I);
+  for (int l = 0; l < cfg_.n_layers; ++l) {
+    const rp_layer_weights& L = layers_[l];
+    char* kpool = kv_ + static_cast<size_t>(l) * layer_kv_bytes_;
+    char* vpool = kv_ + static_cast<size_t>(cfg_.n_layers + l) * layer_kv_bytes_;
+
+    GemmArgs g{};
+    g.A = h; g.lda = H; g.M = M; g.N = nqkv_; g.K = H;
+    g.W = WSeg{{L.wq, L.wk, L.wv}, {nq * hd, nkv * hd, nkv * hd}, 3};
+    g.epi = kEpiPartial; g.splits = s_qkv; g.part = part;
+    HIP_TRY(launch_gemm(bf16_, g, s));
+
+    RopeArgs ra{part, s_qkv, M, L.bq, L.bk, L.bv, nq, nkv, hd, m_pos_, m_slot_, pt, plan_.max_pages,
+                sp<float>(plan_.rope_cos), sp<float>(plan_.rope_sin), q, kpool, vpool};
+    HIP_TRY(launch_rope_append(bf16_, ra, s));
+
+    AttnArgs aa{};
+    aa.q = q; aa.k_pool = kpool; aa.v_pool = vpool; aa.page_table = pt; aa.pt_stride = plan_.max_pages;
+    aa.n_q = nq; aa.n_kv = nkv; aa.hd = hd; aa.scale = 1.0f / std::sqrt(static_cast<float>(hd));
+    aa.n_rows = M; aa.tok_slot = m_slot_; aa.tok_pos = m_pos_;
+    aa.out = attn;
+    if (pre) {
+      aa.n_seq = n_seq; aa.seq_slot = m_seq_slot_; aa.seq_row0 = m_seq_row0_; aa.seq_pos0 = m_seq_pos0_;
+      aa.seq_ntok = m_seq_ntok_; aa.item_off = m_item_off_; aa.total_items = total_items;
+      HIP_TRY(launch_attn_prefill(bf16_, aa, s));
+    } else {
+      aa.B = M; aa.row_slot = m_slot_; aa.row_ctx = m_ctx_; aa.split_off = m_split_off_;
+      aa.total_splits = total_splits; aa.tokens_per_split = tps;
+      aa.part_o = sp<float>(plan_.att_o); aa.part_ml = sp<float>(plan_.att_ml);
+      HIP_TRY(launch_attn_decode(bf16_, aa, s));
+      if (bf16_) HIP_TRY(launch_attn_merge(aa, s));
+    }
+
+    g = GemmArgs{};
+    g.A = attn; g.lda = nq * hd; g.M = M; g.N = H; g.K = nq * hd;
+    g.W = WSeg{{L.wo, nullptr, nullptr}, {H, 0, 0}, 1};
+    g.epi = kEpiPartial; g.splits = s_o; g.part = part;
+    HIP_TRY(launch_gemm(bf16_, g, s));
+
+    AddNormArgs an{x, part, s_o, L.mlp_norm, M, H, eps, h};
+    HIP_TRY(launch_add_rmsnorm(bf16_, an, s));
+
+    g = GemmArgs{};
+    g.A = h; g.lda = H; g.M = M; g.N = I; g.K = H;
+    g.W = WSeg{{L.w_gate, L.w_up, nullptr}, {I, I, 0}, 2};
+    g.epi = kEpiSiluMul; g.splits = 1; g.act_out = act;
+    HIP_TRY(launch_gemm(bf16_, g, s));
+
+    g = GemmArgs{};
+    g.A = act; g.lda = I; g.M = M; g.N = H; g.K = I;
+    g.W = WSeg{{L.w_down, nullptr, nullptr}, {H, 0, 0}, 1};
+    g.epi = kEpiPartial; g.splits = s_d; g.part = part;
+    HIP_TRY(launch_gemm(bf16_, g, s));
+
+    const void* next_norm = (l + 1 < cfg_.n_layers) ? layers_[l + 1].attn_norm : w_.final_norm;
+    AddNormArgs an2{x, part, s_d, next_norm, M, H, eps, h};
+    HIP_TRY(launch_add_rmsnorm(bf16_, an2, s));
+  }
+
+  const void* lm_in = h;
+  int m_lm = M;
+  if (pre) {
+    HIP_TRY(launch_gather_rows(h, m_last_row_, n_seq, H, static_cast<int>(esz_), scratch_ + plan_.hsel, s));
+    lm_in = scratch_ + plan_.hsel;
+    m_lm = n_seq;
+  }
+  GemmArgs g{};
+  g.A = lm_in; g.lda = H; g.M = m_lm; g.N = V; g.K = H;
+  g.W = WSeg{{w_.lm_head, nullptr, nullptr}, {V, 0, 0}, 1};
+  g.epi = kEpiPartial; g.splits = 1; g.part = sp<float>(plan_.logits);
+  HIP_TRY(launch_gemm(bf16_, g, s));
+
+  SampleArgs sa{sp<float>(plan_.logits), m_lm, V, m_gen_slot_, m_gen_pos_, m_gen_hist_,
+                sp<uint64_t>(plan_.slot_seed), sp<uint64_t>(plan_.slot_id), sp<float>(plan_.slot_temp),
+                tokens_cur, sp<int32_t>(plan_.hist), lim_.max_context};
+  HIP_TRY(launch_sample(sa, s));
+}
+
+void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t* toks, const int64_t* offs,
+                               const std::vector<int32_t>& seq_index, float* logits_out) {
+  const int n = static_cast<int>(slots.size());
+  int T = 0;
+  for (int j = 0; j < n; ++j) T += static_cast<int>(offs[seq_index[j] + 1] - offs[seq_index[j]]);
+  const size_t ints = 3 * static_cast<size_t>(T) + 8 * static_cast<size_t>(n) + 1;
+  int32_t* m = stage_meta(ints);
+  int32_t* in_tok = m;
+  int32_t* slot = in_tok + T;
+  int32_t* pos = slot + T;
+  int32_t* seq_slot = pos + T;
+  int32_t* seq_row0 = seq_slot + n;
+  int32_t* seq_pos0 = seq_row0 + n;
+  int32_t* seq_ntok = seq_pos0 + n;
+  int32_t* item_off = seq_ntok + n;
+  int32_t* last_row = item_off + n + 1;
+  int32_t* gen_pos = last_row + n;
+  int32_t* gen_hist = gen_pos + n;
+  const int tpi = attn_prefill_tokens_per_item(bf16_, cfg_.n_q_heads / cfg_.n_kv_heads);
+  int row = 0, items = 0;
+  for (int j = 0; j < n; ++j) {
+    const int64_t o = offs[seq_index[j]];
+    const int p = static_cast<int>(offs[seq_index[j] + 1] - o);
+    for (int t = 0; t < p; ++t) {
+      in_tok[row + t] = toks[o + t];
+      slot[row + t] = slots[j];
+      pos[row + t] = t;
+    }
+    seq_slot[j] = slots[j];
+    seq_row0[j] = row;
+    seq_pos0[j] = 0;
+    seq_ntok[j] = p;
+    item_off[j] = items;
+    items += (p + tpi - 1) / tpi;
+    last_row[j] = row + p - 1;
+    gen_pos[j] = p;
+    gen_hist[j] = 0;
+    row += p;
+  }
+  item_off[n] = items;
+  upload_meta(m, ints);
+  const int32_t* d = d_meta_;
+  m_in_tok_ = d; m_slot_ = d + T; m_pos_ = d + 2 * T;
+  m_seq_slot_ = d + 3 * T; m_seq_row0_ = m_seq_slot_ + n; m_seq_pos0_ = m_seq_row0_ + n;
+  m_seq_ntok_ = m_seq_pos0_ + n; m_item_off_ = m_seq_ntok_ + n; m_last_row_ = m_item_off_ + n + 1;
+  m_gen_pos_ = m_last_row_ + n; m_gen_hist_ = m_gen_pos_ + n; m_gen_slot_ = m_seq_slot_;
+  forward(T, true, n, items, 0, 0);
+  if (logits_out) {
+    HIP_TRY(hipMemcpyAsync(logits_out + static_cast<size_t>(seq_index[0]) * cfg_.vocab, scratch_ + plan_.logits,
+                           static_cast<size_t>(n) * cfg_.vocab * 4, hipMemcpyDeviceToDevice, stream_));
+  }
+}
+
+void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                     const int32_t* max_new, uint64_t seed, float temp, float* logits_out, int32_t* first_out) {
+  check_admission(n, ids, offs, toks, max_new, temp);
+  if (tables_pending_) {
+    HIP_TRY(hipEventSynchronize(ev_tables_));
+    tables_pending_ = false;
+  }
+  std::vector<int32_t> new_slots(n);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = free_slots_.back();
+    free_slots_.pop_back();
+    Seq& q = slots_[s];
+    q = Seq{};
+    q.id = ids[i];
+    q.prompt_len = static_cast<int32_t>(offs[i + 1] - offs[i]);
+    q.max_new = max_new[i];
+    q.seed = seed;
+    q.temp = temp;
+    q.live = true;
+    pool_.take(PagePool::pages_for(q.prompt_len + q.max_new - 1, kPageTokens), s, q.pages);
+    int32_t* row = h_page_table_ + static_cast<size_t>(s) * plan_.max_pages;
+    std::fill(row, row + plan_.max_pages, 0);
+    std::copy(q.pages.begin(), q.pages.end(), row);
+    h_slot_seed_[s] = seed;
+    h_slot_id_[s] = static_cast<uint64_t>(ids[i]);
+    h_slot_temp_[s] = temp;
+    id2slot_[q.id] = s;
+    order_.push_back(s);
+    new_slots[i] = s;
+  }
+  upload_slot_tables();
+  // Chunks of whole prompts with at most max_prefill_tokens tokens.
+  int32_t i = 0;
+  while (i < n) {
+    std::vector<int32_t> cs, ci;
+    int64_t tok = 0;
+    while (i < n) {
+      const int64_t p = offs[i + 1] - offs[i];
+      if (!cs.empty() && tok + p > lim_.max_prefill_tokens) break;
+      cs.push_back(new_slots[i]);
+      ci.push_back(i);
+      tok += p;
+      ++i;
+    }
+    run_prefill_chunk(cs, toks, offs, ci, logits_out);
+  }
+  for (int32_t s : new_slots) {
+    slots_[s].n_gen = 1;
+    if (slots_[s].n_gen >= slots_[s].max_new) slots_[s].finished = true;
+  }
+  if (first_out) {
+    HIP_TRY(hipStreamSynchronize(stream_));
+    std::vector<int32_t> cur(lim_.max_seqs);
+    HIP_TRY(hipMemcpy(cur.data(), scratch_ + plan_.tokens_cur, cur.size() * 4, hipMemcpyDeviceToHost));
+    for (int32_t k = 0; k < n; ++k) first_out[k] = cur[new_slots[k]];
+  }
+}
+
+int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* row_ids_out) {
+  std::vector<int32_t> rows;
+  rows.reserve(order_.size());
+  for (int32_t s : order_)
+    if (!slots_[s].finished) rows.push_back(s);
+  const int B = static_cast<int>(rows.size());
+  if (B == 0) return 0;
+  if (forced) {
+    for (int i = 0; i < B; ++i)
+      if (forced[i] < 0 || forced[i] >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "forced token out of range");
+  }
+  const size_t ints = 7 * static_cast<size_t>(B) + 1;
+  int32_t* m = stage_meta(ints);
+  int32_t* in_tok = m;
+  int32_t* slot = in_tok + B;
+  int32_t* pos = slot + B;
+  int32_t* ctx = pos + B;
+  int32_t* split_off = ctx + B;
+  int32_t* gen_pos = split_off + B + 1;
+  int32_t* gen_hist = gen_pos + B;
+  int64_t total_pages = 0;
+  for (int i = 0; i < B; ++i) {
+    const Seq& q = slots_[rows[i]];
+    in_tok[i] = forced ? forced[i] : -1;
+    slot[i] = rows[i];
+    pos[i] = q.prompt_len + q.n_gen - 1;
+    ctx[i] = pos[i] + 1;
+    gen_pos[i] = pos[i] + 1;
+    gen_hist[i] = q.n_gen;
+    total_pages += PagePool::pages_for(ctx[i], kPageTokens);
+  }
+  int tps = 0, total_splits = 0;
+  if (bf16_) {
+    const int64_t target = decode_split_target(cfg_);
+    const int64_t pps = std::max<int64_t>(1, (total_pages + target - 1) / target);
+    tps = static_cast<int>(pps * kPageTokens);
+    for (int i = 0; i < B; ++i) {
+      split_off[i] = total_splits;
+      total_splits += (ctx[i] + tps - 1) / tps;
+    }
+    if (total_splits > plan_.split_cap) throw RpError(RP_ERR_CAPACITY, "decode split capacity exceeded");
+  } else {
+    for (int i = 0; i < B; ++i) split_off[i] = 0;
+  }
+  split_off[B] = total_splits;
+  upload_meta(m, ints);
+  const int32_t* d = d_meta_;
+  m_in_tok_ = d; m_slot_ = d + B; m_pos_ = d + 2 * B; m_ctx_ = d + 3 * B; m_split_off_ = d + 4 * B;
+  m_gen_pos_ = d + 5 * B + 1; m_gen_hist_ = d + 6 * B + 1; m_gen_slot_ = m_slot_;
+  forward(B, false, 0, 0, total_splits, tps);
+  if (logits_out) {
+    HIP_TRY(hipMemcpyAsync(logits_out, scratch_ + plan_.logits, static_cast<size_t>(B) * cfg_.vocab * 4,
+                           hipMemcpyDeviceToDevice, stream_));
+  }
+  for (int i = 0; i < B; ++i) {
+    Seq& q = slots_[rows[i]];
+    if (row_ids_out) row_ids_out[i] = q.id;
+    q.n_gen += 1;
+    if (q.n_gen >= q.max_new) q.finished = true;
+  }
+  return B;
+}
+
+void Engine::release(int32_t slot) {
+  Seq& q = slots_[slot];
+  pool_.give_back(q.pages, slot);
+  id2slot_.erase(q.id);
+  order_.erase(std::find(order_.begin(), order_.end(), slot));
+  free_slots_.push_back(slot);
+  q = Seq{};
+}
+
+int32_t Engine::free_finished(int64_t* ids_out, int32_t cap) {
+  std::vector<int32_t> fin;
+  for (int32_t s : order_)
+    if (slots_[s].finished && static_cast<int32_t>(fin.size()) < cap) fin.push_back(s);
+  for (size_t k = 0; k < fin.size(); ++k) {
+    if (ids_out) ids_out[k] = slots_[fin[k]].id;
+    release(fin[k]);
+  }
+  return static_cast<int32_t>(fin.size());
+}
+
+void Engine::abort(int32_t n, const int64_t* ids) {
+  if (n < 0 || (n > 0 && !ids)) throw RpError(RP_ERR_INVALID_ARG, "abort: bad arguments");
+  std::unordered_map<int64_t, int> seen;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!id2slot_.count(ids[i])) throw RpError(RP_ERR_UNKNOWN_ID, "abort: unknown sequence id");
+    if (seen.count(ids[i])) throw RpError(RP_ERR_INVALID_ARG, "abort: duplicate id");
+    seen[ids[i]] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i) release(id2slot_.at(ids[i]));
+}
+
+int32_t Engine::get_tokens(int64_t id, int32_t* out, int32_t cap) {
+  auto it = id2slot_.find(id);
+  if (it == id2slot_.end()) throw RpError(RP_ERR_UNKNOWN_ID, "get_tokens: unknown sequence id");
+  const Seq& q = slots_[it->second];
+  HIP_TRY(hipStreamSynchronize(stream_));
+  const int32_t k = std::min(cap, q.n_gen);
+  if (k > 0) {
+    if (!out) throw RpError(RP_ERR_INVALID_ARG, "get_tokens: null output");
+    HIP_TRY(hipMemcpy(out, sp<int32_t>(plan_.hist) + static_cast<size_t>(it->second) * lim_.max_context, k * 4,
+                      hipMemcpyDeviceToHost));
+  }
+  return q.n_gen;
+}
+
+int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                        const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
+                        int32_t* resp_out, rp_round_stats* stats, int32_t max_stats) {
+  if (!order_.empty()) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
+  if (n < 1 || !ids || !toks || !offs || !max_new || !resp_out)
+    throw RpError(RP_ERR_INVALID_ARG, "rollout: null array or n < 1");
+  if (!(temp >= 0.f) || std::isinf(temp)) throw RpError(RP_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+  if (offs[0] != 0) throw RpError(RP_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
+  std::unordered_map<int64_t, int> seen;
+  std::vector<int64_t> resp_off(n + 1, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const int64_t p = offs[i + 1] - offs[i];
+    if (p < 1 || max_new[i] < 1) throw RpError(RP_ERR_INVALID_ARG, "prompts and max_new_tokens must be >= 1");
+    if (p > lim_.max_prefill_tokens || p + max_new[i] - 1 > lim_.max_context)
+      throw RpError(RP_ERR_CAPACITY, "a sequence exceeds max_prefill_tokens or max_context");
+    if (PagePool::pages_for(p + max_new[i] - 1, kPageTokens) > pool_.capacity())
+      throw RpError(RP_ERR_OUT_OF_PAGES, "a sequence needs more pages than the pool holds");
+    if (seen.count(ids[i])) throw RpError(RP_ERR_DUPLICATE_ID, "duplicate sequence id");
+    seen[ids[i]] = 1;
+    for (int64_t t = offs[i]; t < offs[i + 1]; ++t)
+      if (toks[t] < 0 || toks[t] >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "prompt token id out of range");
+    resp_off[i + 1] = resp_off[i] + max_new[i];
+  }
+  std::map<int32_t, std::vector<int32_t>> rounds;
+  for (int32_t i = 0; i < n; ++i) rounds[round_ids ? round_ids[i] : 0].push_back(i);
+
+  const size_t resp_cap = static_cast<size_t>(lim_.max_seqs) * lim_.max_context;
+  int32_t* resp_dev = sp<int32_t>(plan_.resp);
+  const int32_t* hist = sp<int32_t>(plan_.hist);
+  auto event_at = [&](size_t k) {
+    while (events_.size() <= k) {
+      hipEvent_t e;
+      HIP_TRY(hipEventCreate(&e));
+      events_.push_back(e);
+    }
+    return events_[k];
+  };
+
+  int32_t r_idx = 0;
+  for (auto& kv : rounds) {
+    const std::vector<int32_t>& members = kv.second;
+    size_t next = 0;
+    size_t n_ev = 0;
+    hipEvent_t ev_start = event_at(n_ev++);
+    hipEvent_t ev_pre = event_at(n_ev++);
+    hipEvent_t ev_end = event_at(n_ev++);
+    std::vector<std::pair<size_t, int32_t>> finish_ev;  // (event index, member position)
+    std::vector<std::array<int64_t, 3>> pending_copies;  // dev offset, host offset, length
+    size_t resp_cursor = 0;
+    std::unordered_map<int32_t, int32_t> slot_member;
+    pool_.reset_peak();
+    int32_t steps = 0;
+    int64_t prompt_tokens = 0, gen_tokens = 0;
+
+    auto flush = [&]() {
+      if (pending_copies.empty()) return;
+      HIP_TRY(hipStreamSynchronize(stream_));
+      for (auto& c : pending_copies)
+        HIP_TRY(hipMemcpy(resp_out + c[1], resp_dev + c[0], static_cast<size_t>(c[2]) * 4, hipMemcpyDeviceToHost));
+      pending_copies.clear();
+      resp_cursor = 0;
+    };
+    auto admit = [&]() {
+      std::vector<int64_t> b_ids, b_offs{0};
+      std::vector<int32_t> b_toks, b_new, b_mem;
+      int64_t pages = 0;
+      while (next < members.size() && b_ids.size() < free_slots_.size()) {
+        const int32_t i = members[next];
+        const int64_t need = PagePool::pages_for(offs[i + 1] - offs[i] + max_new[i] - 1, kPageTokens);
+        if (!pool_.can_take(pages + need)) break;
+        pages += need;
+        b_ids.push_back(ids[i]);
+        b_toks.insert(b_toks.end(), toks + offs[i], toks + offs[i + 1]);
+        b_offs.push_back(static_cast<int64_t>(b_toks.size()));
+        b_new.push_back(max_new[i]);
+        b_mem.push_back(i);
+        prompt_tokens += offs[i + 1] - offs[i];
+        ++next;
+      }
+      if (b_ids.empty()) return;
+      const size_t before = order_.size();
+      prefill(static_cast<int32_t>(b_ids.size()), b_ids.data(), b_toks.data(), b_offs.data(), b_new.data(), seed,
+              temp, nullptr, nullptr);
+      for (size_t k = 0; k < b_mem.size(); ++k) slot_member[order_[before + k]] = b_mem[k];
+    };
+    auto collect_finished = [&]() {
+      bool any = false;
+      for (int32_t s : order_) {
+        if (!slots_[s].finished) continue;
+        const int32_t i = slot_member.at(s);
+        const int64_t len = max_new[i];
+        if (resp_cursor + len > resp_cap) flush();
+        HIP_TRY(hipMemcpyAsync(resp_dev + resp_cursor, hist + static_cast<size_t>(s) * lim_.max_context, len * 4,
+                               hipMemcpyDeviceToDevice, stream_));
+        pending_copies.push_back({static_cast<int64_t>(resp_cursor), resp_off[i], len});
+        resp_cursor += len;
+        finish_ev.push_back({n_ev, i});
+        gen_tokens += len;
+        any = true;
+      }
+      if (any) {
+        HIP_TRY(hipEventRecord(event_at(n_ev), stream_));
+        ++n_ev;
+        for (int32_t s : std::vector<int32_t>(order_))
+          if (slots_[s].finished) {
+            slot_member.erase(s);
+            release(s);
+          }
+      }
+    };
+
+    HIP_TRY(hipEventRecord(ev_start, stream_));
+    admit();
+    HIP_TRY(hipEventRecord(ev_pre, stream_));
+    collect_finished();
+    while (true) {
+      if (next < members.size()) {
+        admit();
+        collect_finished();
+      }
+      if (order_.empty() && next >= members.size()) break;
+      if (order_.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "rollout: a sequence cannot be admitted");
+      decode_step(nullptr, nullptr, nullptr);
+      ++steps;
+      collect_finished();
+    }
+    HIP_TRY(hipEventRecord(ev_end, stream_));
+    flush();
+    HIP_TRY(hipEventSynchronize(ev_end));
+
+    if (stats && r_idx < max_stats) {
+      rp_round_stats& st = stats[r_idx];
+      st = rp_round_stats{};
+      float ms = 0.f;
+      st.round_id = kv.first;
+      st.n_seqs = static_cast<int32_t>(members.size());
+      st.decode_steps = steps;
+      st.prompt_tokens = prompt_tokens;
+      st.generated_tokens = gen_tokens;
+      st.peak_pages = pool_.peak_used();
+      HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_end));
+      st.makespan_ms = ms;
+      HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_pre));
+      st.prefill_ms = ms;
+      st.decode_ms = st.makespan_ms - st.prefill_ms;
+      double idle = 0.0;
+      for (auto& fe : finish_ev) {
+        HIP_TRY(hipEventElapsedTime(&ms, events_[fe.first], ev_end));
+        idle += std::max(0.0, static_cast<double>(ms)) * 1e-3;
+      }
+      st.idle_slot_s = idle;
+      const double denom = static_cast<double>(members.size()) * st.makespan_ms * 1e-3;
+      st.slot_idle = denom > 0 ? idle / denom : 0.0;
+    }
+    ++r_idx;
+  }
+  return r_idx;
+}
+
+}  // namespace rollpack

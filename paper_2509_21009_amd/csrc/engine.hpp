@@ -1,0 +1,136 @@
+// Rollout engine: host-side state and step loop of the C ABI in rollpack.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <stdexcept>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/rollpack.h"
+#include "kernels.hpp"
+#include "kv_pool.hpp"
+
+namespace rollpack {
+
+struct RpError : std::runtime_error {
+  rp_status status;
+  RpError(rp_status s, const std::string& m) : std::runtime_error(m), status(s) {}
+};
+
+// Byte offsets of every buffer carved from the caller's scratch workspace.
+struct ScratchPlan {
+  size_t x, h, part, q, attn, act, hsel, logits, att_o, att_ml, rope_cos, rope_sin, page_table,
+      tokens_cur, hist, resp, slot_seed, slot_id, slot_temp, meta;
+  size_t total;
+  size_t part_elems;
+  int32_t split_cap;   // decode attention work-item capacity (splits)
+  int32_t max_pages;   // page-table row width
+  int32_t meta_ints;
+};
+
+ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l);
+size_t kv_pool_bytes(const rp_model_config& c, int64_t pages);
+void validate_config(const rp_model_config& c);
+void validate_limits(const rp_engine_limits& l);
+
+struct Seq {
+  int64_t id = -1;
+  int32_t prompt_len = 0;
+  int32_t max_new = 0;
+  int32_t n_gen = 0;     // tokens sampled so far
+  uint64_t seed = 0;
+  float temp = 0.f;
+  bool live = false;
+  bool finished = false;
+  std::vector<int32_t> pages;
+};
+
+struct RoundInput {
+  std::vector<int32_t> idx;  // indices into the call's arrays
+};
+
+class Engine {
+ public:
+  Engine(const rp_model_config& cfg, const rp_weights& w, const rp_engine_limits& lim, void* kv_ws,
+         size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, hipStream_t stream);
+  ~Engine();
+
+  void prefill(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+               const int32_t* max_new, uint64_t seed, float temp, float* logits_out, int32_t* first_out);
+  int32_t decode_step(const int32_t* forced, float* logits_out, int64_t* row_ids_out);
+  int32_t free_finished(int64_t* ids_out, int32_t cap);
+  void abort(int32_t n, const int64_t* ids);
+  int32_t get_tokens(int64_t id, int32_t* out, int32_t cap);
+  int32_t rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                  const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
+                  int32_t* resp_out, rp_round_stats* stats, int32_t max_stats);
+
+  bool broken() const { return broken_; }
+  void mark_broken() { broken_ = true; }
+  int32_t live_count() const { return static_cast<int32_t>(order_.size()); }
+
+ private:
+  struct Staging {
+    void* host = nullptr;
+    hipEvent_t ev = nullptr;
+    bool pending = false;
+  };
+
+  void forward(int M, bool is_prefill, int n_seq_prefill, int total_items, int total_splits, int tps);
+  int32_t* stage_meta(size_t ints);
+  void upload_meta(const int32_t* host, size_t ints);
+  void upload_slot_tables();
+  void check_admission(int32_t n, const int64_t* ids, const int64_t* offs, const int32_t* toks,
+                       const int32_t* max_new, float temp) const;
+  void run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t* toks, const int64_t* offs,
+                         const std::vector<int32_t>& seq_index, float* logits_out);
+  void release(int32_t slot);
+  template <typename T> T* sp(size_t off) const { return reinterpret_cast<T*>(scratch_ + off); }
+
+  rp_model_config cfg_;
+  rp_engine_limits lim_;
+  std::vector<rp_layer_weights> layers_;
+  rp_weights w_;
+  hipStream_t stream_;
+  bool bf16_;
+  size_t esz_;
+  int nqkv_;
+  ScratchPlan plan_;
+  char* kv_;
+  char* scratch_;
+  size_t layer_kv_bytes_;  // bytes of one layer's K (or V) pool
+  PagePool pool_;
+  std::vector<Seq> slots_;
+  std::vector<int32_t> free_slots_;
+  std::vector<int32_t> order_;  // live slots in admission order
+  std::unordered_map<int64_t, int32_t> id2slot_;
+  // pinned host mirrors
+  int32_t* h_page_table_ = nullptr;
+  uint64_t* h_slot_seed_ = nullptr;
+  uint64_t* h_slot_id_ = nullptr;
+  float* h_slot_temp_ = nullptr;
+  hipEvent_t ev_tables_ = nullptr;
+  bool tables_pending_ = false;
+  std::vector<Staging> ring_;
+  size_t ring_next_ = 0;
+  size_t ring_bytes_ = 0;
+  bool broken_ = false;
+  // device metadata views (set by the last stage/upload)
+  const int32_t* d_meta_ = nullptr;
+  // metadata pointers used by forward()
+  const int32_t *m_in_tok_ = nullptr, *m_slot_ = nullptr, *m_pos_ = nullptr, *m_hist_ = nullptr,
+                *m_ctx_ = nullptr, *m_split_off_ = nullptr, *m_seq_slot_ = nullptr,
+                *m_seq_row0_ = nullptr, *m_seq_pos0_ = nullptr, *m_seq_ntok_ = nullptr,
+                *m_item_off_ = nullptr, *m_last_row_ = nullptr, *m_gen_pos_ = nullptr,
+                *m_gen_hist_ = nullptr, *m_gen_slot_ = nullptr;
+  std::vector<hipEvent_t> events_;
+};
+
+}  // namespace rollpack
+
+struct rp_engine {
+  rollpack::Engine* impl;
+};

@@ -1,0 +1,320 @@
+// Causal GQA attention over the paged KV cache.
+//
+// One 64-lane wave owns a work item: up to 16 query rows that share one KV
+// head (the G query heads of a token, or G heads x floor(16/G) tokens in
+// prefill) and a range of KV tokens.  Per 64-token page it computes
+// S^T = K Q^T as four 16x16 MFMA tiles, runs an online softmax in the log2
+// domain, and accumulates O^T = V^T P^T with MFMA.  V pages are stored
+// transposed ([hd][64 tokens]) so both MFMA operands are read as contiguous
+// 16-byte runs straight from HBM; the page's tokens are assigned to MFMA
+// rows so that each lane's softmax outputs are exactly the P^T operand it
+// must supply, with no data exchange between lanes.
+//
+// Decode splits each sequence's context into chunks (one work item each) so
+// that small batches with long contexts still spread over all CUs; a merge
+// kernel combines the chunk maxima, sums and partial outputs.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace rollpack {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Token (within a 64-token page) that MFMA row i of S^T tile t stands for.
+__device__ __forceinline__ int tile_token(int t, int i) {
+  return 32 * (t >> 1) + 8 * (i >> 2) + 4 * (t & 1) + (i & 3);
+}
+
+struct SoftmaxState {
+  float m, l;
+};
+
+// Process one page for the 16 rows of a wave.  qf: query operands;
+// row_lim: last key position row c may see (inclusive); t_lo/t_hi: the
+// item's key range [t_lo, t_hi).
+template <int HD>
+__device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, int page_tok0,
+                                            const bf16x8_t (&qf)[HD / 32], int row_lim, int t_lo,
+                                            int t_hi, float scale_log2, SoftmaxState& st,
+                                            f32x4_t (&o)[HD / 16]) {
+  constexpr int KS = HD / 32, HQ = HD / 4;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  f32x4_t sacc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const bf16_t* krow = kb + tile_token(t, c) * HD + g * HQ;
+    bf16x8_t kf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = load_bf16x8(krow + ks * 8);
+    sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) sacc[t] = mfma16x16x32(kf[ks], qf[ks], sacc[t]);
+  }
+  bf16x8_t vf[HD / 16][2];
+#pragma unroll
+  for (int blk = 0; blk < HD / 16; ++blk)
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) vf[blk][pp] = load_bf16x8(vb + (blk * 16 + c) * kPageTokens + 32 * pp + 8 * g);
+
+  float sv[16];
+  float pmax = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int tok = page_tok0 + 32 * (t >> 1) + 8 * g + 4 * (t & 1) + e;
+      float v = sacc[t][e] * scale_log2;
+      if (tok < t_lo || tok >= t_hi || tok > row_lim) v = -INFINITY;
+      sv[t * 4 + e] = v;
+      pmax = fmaxf(pmax, v);
+    }
+  pmax = fmaxf(pmax, __shfl_xor(pmax, 16, 64));
+  pmax = fmaxf(pmax, __shfl_xor(pmax, 32, 64));
+  const float m_new = fmaxf(st.m, pmax);
+  const float shift = (m_new == -INFINITY) ? 0.f : m_new;
+  const float alpha = exp2f(st.m - shift);
+  float psum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    sv[i] = exp2f(sv[i] - shift);
+    psum += sv[i];
+  }
+  psum += __shfl_xor(psum, 16, 64);
+  psum += __shfl_xor(psum, 32, 64);
+  st.l = st.l * alpha + psum;
+  st.m = m_new;
+  bf16x8_t pf[2];
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    uint4 w;
+    w.x = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 0])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 1])) << 16);
+    w.y = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 2])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 3])) << 16);
+    w.z = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 4])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 5])) << 16);
+    w.w = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 6])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 7])) << 16);
+    pf[pp] = __builtin_bit_cast(bf16x8_t, w);
+  }
+#pragma unroll
+  for (int blk = 0; blk < HD / 16; ++blk) {
+    o[blk] = o[blk] * alpha;
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) o[blk] = mfma16x16x32(vf[blk][pp], pf[pp], o[blk]);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
+  constexpr int KS = HD / 32, HQ = HD / 4;
+  const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+  const int x = blockIdx.x, kh = blockIdx.y;
+  int lo = 0, hi = a.B;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (a.split_off[mid] <= x) lo = mid; else hi = mid;
+  }
+  const int b = lo;
+  const int s = x - a.split_off[b];
+  const int ctx = a.row_ctx[b];
+  const int t0 = s * a.tokens_per_split;
+  const int t1 = min(t0 + a.tokens_per_split, ctx);
+  const int slot = a.row_slot[b];
+  const int G = a.n_q / a.n_kv;
+
+  bf16x8_t qf[KS];
+  if (c < G) {
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (static_cast<size_t>(b) * a.n_q + kh * G + c) * HD + g * HQ;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 8);
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
+  }
+  f32x4_t o[HD / 16];
+#pragma unroll
+  for (int blk = 0; blk < HD / 16; ++blk) o[blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  SoftmaxState st{-INFINITY, 0.f};
+  const bf16_t* kpool = static_cast<const bf16_t*>(a.k_pool);
+  const bf16_t* vpool = static_cast<const bf16_t*>(a.v_pool);
+  const float scale_log2 = a.scale * kLog2e;
+  const int* pt = a.page_table + static_cast<size_t>(slot) * a.pt_stride;
+  for (int p = t0 / kPageTokens; p * kPageTokens < t1; ++p) {
+    const size_t pb = (static_cast<size_t>(pt[p]) * a.n_kv + kh) * kPageTokens * HD;
+    attend_page<HD>(kpool + pb, vpool + pb, p * kPageTokens, qf, 0x7fffffff, t0, t1, scale_log2, st, o);
+  }
+  const size_t item = static_cast<size_t>(x) * a.n_kv + kh;
+  if (c < G) {
+    float* po = a.part_o + (item * 16 + c) * HD;
+#pragma unroll
+    for (int blk = 0; blk < HD / 16; ++blk)
+      *reinterpret_cast<float4*>(po + blk * 16 + 4 * g) = make_float4(o[blk][0], o[blk][1], o[blk][2], o[blk][3]);
+    if (g == 0) {
+      a.part_ml[item * 32 + c] = st.m;
+      a.part_ml[item * 32 + 16 + c] = st.l;
+    }
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(128) void k_attn_merge(AttnArgs a) {
+  const int b = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+  const int G = a.n_q / a.n_kv;
+  const int kh = h / G, c = h % G;
+  const int s0 = a.split_off[b], s1 = a.split_off[b + 1];
+  float mx = -INFINITY;
+  for (int s = s0; s < s1; ++s) mx = fmaxf(mx, a.part_ml[(static_cast<size_t>(s) * a.n_kv + kh) * 32 + c]);
+  float num = 0.f, den = 0.f;
+  for (int s = s0; s < s1; ++s) {
+    const size_t item = static_cast<size_t>(s) * a.n_kv + kh;
+    const float ms = a.part_ml[item * 32 + c];
+    if (ms == -INFINITY) continue;
+    const float w = exp2f(ms - mx);
+    den += w * a.part_ml[item * 32 + 16 + c];
+    if (d < HD) num += w * a.part_o[(item * 16 + c) * HD + d];
+  }
+  if (d < HD)
+    static_cast<bf16_t*>(a.out)[(static_cast<size_t>(b) * a.n_q + h) * HD + d] = f32_to_bf16(num / den);
+}
+
+template <int HD>
+__global__ __launch_bounds__(64) void k_attn_prefill_bf16(AttnArgs a, int tpi) {
+  constexpr int KS = HD / 32, HQ = HD / 4;
+  const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+  const int x = blockIdx.x, kh = blockIdx.y;
+  int lo = 0, hi = a.n_seq;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (a.item_off[mid] <= x) lo = mid; else hi = mid;
+  }
+  const int j = lo;
+  const int qb = x - a.item_off[j];
+  const int ntok = a.seq_ntok[j];
+  const int G = a.n_q / a.n_kv;
+  const int tq = qb * tpi + c / G;
+  const bool valid = c < tpi * G && tq < ntok;
+  const int head = kh * G + c % G;
+  const int pos0 = a.seq_pos0[j];
+  const int row_lim = valid ? pos0 + tq : -1;
+  const int last_tok = min(qb * tpi + tpi, ntok) - 1;
+  const int t_end = pos0 + last_tok + 1;
+  const size_t qrow_idx = static_cast<size_t>(a.seq_row0[j] + tq);
+
+  bf16x8_t qf[KS];
+  if (valid) {
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (qrow_idx * a.n_q + head) * HD + g * HQ;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 8);
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
+  }
+  f32x4_t o[HD / 16];
+#pragma unroll
+  for (int blk = 0; blk < HD / 16; ++blk) o[blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  SoftmaxState st{-INFINITY, 0.f};
+  const bf16_t* kpool = static_cast<const bf16_t*>(a.k_pool);
+  const bf16_t* vpool = static_cast<const bf16_t*>(a.v_pool);
+  const float scale_log2 = a.scale * kLog2e;
+  const int* pt = a.page_table + static_cast<size_t>(a.seq_slot[j]) * a.pt_stride;
+  for (int p = 0; p * kPageTokens < t_end; ++p) {
+    const size_t pb = (static_cast<size_t>(pt[p]) * a.n_kv + kh) * kPageTokens * HD;
+    attend_page<HD>(kpool + pb, vpool + pb, p * kPageTokens, qf, row_lim, 0, t_end, scale_log2, st, o);
+  }
+  if (valid) {
+    const float inv = 1.0f / st.l;
+    bf16_t* out = static_cast<bf16_t*>(a.out) + (qrow_idx * a.n_q + head) * HD;
+#pragma unroll
+    for (int blk = 0; blk < HD / 16; ++blk) {
+      uint2 pk;
+      pk.x = static_cast<uint32_t>(f32_to_bf16(o[blk][0] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[blk][1] * inv)) << 16);
+      pk.y = static_cast<uint32_t>(f32_to_bf16(o[blk][2] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[blk][3] * inv)) << 16);
+      *reinterpret_cast<uint2*>(out + blk * 16 + 4 * g) = pk;
+    }
+  }
+}
+
+// fp32 model: one wave per (row, query head), one key at a time.
+__global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
+  const int i = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int HD = a.hd;
+  const int G = a.n_q / a.n_kv, kh = h / G;
+  const int slot = a.tok_slot[i], pos = a.tok_pos[i];
+  const float* q = static_cast<const float*>(a.q) + (static_cast<size_t>(i) * a.n_q + h) * HD;
+  const float* kpool = static_cast<const float*>(a.k_pool);
+  const float* vpool = static_cast<const float*>(a.v_pool);
+  const int* pt = a.page_table + static_cast<size_t>(slot) * a.pt_stride;
+  float qv[2] = {lane < HD ? q[lane] : 0.f, lane + 64 < HD ? q[lane + 64] : 0.f};
+  float acc[2] = {0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  for (int t = 0; t <= pos; ++t) {
+    const size_t pb = (static_cast<size_t>(pt[t / kPageTokens]) * a.n_kv + kh) * kPageTokens * HD;
+    const int off = t % kPageTokens;
+    const float* k = kpool + pb + static_cast<size_t>(off) * HD;
+    float part = (lane < HD ? qv[0] * k[lane] : 0.f) + (lane + 64 < HD ? qv[1] * k[lane + 64] : 0.f);
+    const float s = wave_sum(part) * a.scale;
+    const float m_new = fmaxf(m, s);
+    const float alpha = expf(m - m_new);
+    const float p = expf(s - m_new);
+    l = l * alpha + p;
+    m = m_new;
+    const float* v = vpool + pb;
+    if (lane < HD) acc[0] = acc[0] * alpha + p * v[static_cast<size_t>(lane) * kPageTokens + off];
+    if (lane + 64 < HD) acc[1] = acc[1] * alpha + p * v[static_cast<size_t>(lane + 64) * kPageTokens + off];
+  }
+  float* out = static_cast<float*>(a.out) + (static_cast<size_t>(i) * a.n_q + h) * HD;
+  if (lane < HD) out[lane] = acc[0] / l;
+  if (lane + 64 < HD) out[lane + 64] = acc[1] / l;
+}
+
+}  // namespace
+
+int attn_prefill_tokens_per_item(int bf16, int group) {
+  if (!bf16) return 1;
+  const int t = 16 / group;
+  return t < 1 ? 1 : t;
+}
+
+hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s) {
+  if (!bf16) {
+    if (a.n_rows <= 0) return hipSuccess;
+    if (a.hd > 128) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_attn_f32, dim3(a.n_rows, a.n_q), dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.B <= 0 || a.total_splits <= 0) return hipSuccess;
+  if (a.n_q / a.n_kv > 16 || a.tokens_per_split % kPageTokens != 0) return hipErrorInvalidValue;
+  dim3 grid(a.total_splits, a.n_kv);
+  if (a.hd == 128) hipLaunchKernelGGL(k_attn_decode_bf16<128>, grid, dim3(64), 0, s, a);
+  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_decode_bf16<64>, grid, dim3(64), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_merge(const AttnArgs& a, hipStream_t s) {
+  if (a.B <= 0) return hipSuccess;
+  dim3 grid(a.B, a.n_q);
+  if (a.hd == 128) hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(128), 0, s, a);
+  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_merge<64>, grid, dim3(128), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_prefill(int bf16, const AttnArgs& a, hipStream_t s) {
+  if (!bf16) {
+    if (a.n_rows <= 0) return hipSuccess;
+    if (a.hd > 128) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_attn_f32, dim3(a.n_rows, a.n_q), dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.total_items <= 0) return hipSuccess;
+  const int G = a.n_q / a.n_kv;
+  if (G > 16) return hipErrorInvalidValue;
+  const int tpi = attn_prefill_tokens_per_item(1, G);
+  dim3 grid(a.total_items, a.n_kv);
+  if (a.hd == 128) hipLaunchKernelGGL(k_attn_prefill_bf16<128>, grid, dim3(64), 0, s, a, tpi);
+  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_prefill_bf16<64>, grid, dim3(64), 0, s, a, tpi);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace rollpack

@@ -1,0 +1,367 @@
+// Dense projections C[m, n] = sum_k A[m, k] * W[n, k] of the decoder
+// (q/k/v, o, gate/up, down, LM head).  W is [out, in] row-major, A is the
+// [M, K] activation matrix; both are K-contiguous.
+//
+// bf16 kernels use gfx950 MFMA (v_mfma_f32_16x16x32_bf16) with fp32
+// accumulation and W as the 16-row "A" operand, activations as the
+// 16-column "B" operand, so one MFMA yields a [16 n, 16 m] tile of C^T.
+//
+//  * k_gemm_stream (M <= 64, the decode regime): the weights are streamed
+//    once from HBM straight into registers; every lane loads 64 contiguous
+//    bytes per row per 128-wide K chunk (the K order inside a chunk is
+//    permuted identically for both operands, which leaves the dot products
+//    unchanged).  The 4 waves of a block split the chunk range and reduce
+//    through LDS; blockIdx.y splits K further and writes fp32 partials that
+//    the consumer kernel sums.
+//  * k_gemm_tiled (M > 64: prefill and large decode batches): 128x128 block
+//    tiles staged through padded LDS, 2x2 waves of 64x64, register prefetch
+//    of the next K block.
+//  * k_gemm_f32: fp32 FMA tiles for the fp32 model (no reduced precision).
+//
+// The SiLU epilogue pairs gate row i with up row i in one thread and writes
+// silu(gate) * up once, rounded to the storage type.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace rollpack {
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ const T* seg_row(const WSeg& W, int n, int K) {
+  int base = 0;
+  for (int s = 0; s < 3; ++s) {
+    if (s == W.n_seg - 1 || n < base + W.rows[s])
+      return static_cast<const T*>(W.ptr[s]) + static_cast<size_t>(n - base) * K;
+    base += W.rows[s];
+  }
+  return static_cast<const T*>(W.ptr[0]);
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// ---- decode-regime weight streaming ----------------------------------------
+template <int R, int MT, bool SILU>
+__global__ __launch_bounds__(256) void k_gemm_stream(GemmArgs a, int chunks_per_split) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, r = lane & 15;
+  const int K = a.K;
+  const bf16_t* wrow[R];
+#pragma unroll
+  for (int t = 0; t < R; ++t) {
+    if (SILU) {
+      wrow[t] = static_cast<const bf16_t*>(a.W.ptr[t]) + static_cast<size_t>(blockIdx.x * 16 + r) * K;
+    } else {
+      wrow[t] = seg_row<bf16_t>(a.W, (blockIdx.x * R + t) * 16 + r, K);
+    }
+  }
+  const bf16_t* arow[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    int m = mt * 16 + r;
+    if (m >= a.M) m = a.M - 1;
+    arow[mt] = static_cast<const bf16_t*>(a.A) + static_cast<size_t>(m) * a.lda;
+  }
+  f32x4_t acc[R][MT];
+#pragma unroll
+  for (int t = 0; t < R; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int n_chunks = K / 128;
+  const int c0 = blockIdx.y * chunks_per_split;
+  const int c1 = min(c0 + chunks_per_split, n_chunks);
+  for (int c = c0 + wave; c < c1; c += 4) {
+    const int k = c * 128 + g * 32;
+    bf16x8_t wv[R][4], av[MT][4];
+#pragma unroll
+    for (int t = 0; t < R; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) wv[t][j] = load_bf16x8(wrow[t] + k + 8 * j);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) av[mt][j] = load_bf16x8(arow[mt] + k + 8 * j);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int t = 0; t < R; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] = mfma16x16x32(wv[t][j], av[mt][j], acc[t][mt]);
+  }
+
+  constexpr int NSL = R * MT * 4;
+  __shared__ float red[4][NSL][64];
+#pragma unroll
+  for (int t = 0; t < R; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) red[wave][(t * MT + mt) * 4 + e][lane] = acc[t][mt][e];
+  __syncthreads();
+
+  if (!SILU) {
+    for (int q = threadIdx.x; q < NSL * 64; q += 256) {
+      const int ln = q & 63, sl = q >> 6;
+      const int e = sl & 3, tm = sl >> 2, mt = tm % MT, t = tm / MT;
+      const int m = mt * 16 + (ln & 15);
+      if (m < a.M) {
+        const float v = red[0][sl][ln] + red[1][sl][ln] + red[2][sl][ln] + red[3][sl][ln];
+        const int n = (blockIdx.x * R + t) * 16 + (ln >> 4) * 4 + e;
+        a.part[(static_cast<size_t>(blockIdx.y) * a.M + m) * a.N + n] = v;
+      }
+    }
+  } else {
+    bf16_t* out = static_cast<bf16_t*>(a.act_out);
+    for (int q = threadIdx.x; q < MT * 4 * 64; q += 256) {
+      const int ln = q & 63, sl = q >> 6;
+      const int e = sl & 3, mt = sl >> 2;
+      const int m = mt * 16 + (ln & 15);
+      if (m < a.M) {
+        const int sg = mt * 4 + e, su = (MT + mt) * 4 + e;
+        const float gv = red[0][sg][ln] + red[1][sg][ln] + red[2][sg][ln] + red[3][sg][ln];
+        const float uv = red[0][su][ln] + red[1][su][ln] + red[2][su][ln] + red[3][su][ln];
+        const int i = blockIdx.x * 16 + (ln >> 4) * 4 + e;
+        out[static_cast<size_t>(m) * a.N + i] = f32_to_bf16(silu(gv) * uv);
+      }
+    }
+  }
+}
+
+// ---- prefill / large-batch tiled MFMA GEMM ---------------------------------
+constexpr int kTBN = 128, kTBM = 128, kTBK = 64, kTLDK = kTBK + 8;
+
+template <bool SILU>
+__global__ __launch_bounds__(256) void k_gemm_tiled(GemmArgs a, int kblocks_per_split) {
+  __shared__ __attribute__((aligned(16))) bf16_t Ws[kTBN * kTLDK];
+  __shared__ __attribute__((aligned(16))) bf16_t As[kTBM * kTLDK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r = lane & 15;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int bn = blockIdx.x, bm = blockIdx.y, split = blockIdx.z;
+  const int K = a.K;
+
+  const bf16_t* wsrc[4];
+  const bf16_t* asrc[4];
+  int lds_off[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int q = tid + 256 * i;
+    const int row = q >> 3, col = (q & 7) * 8;
+    if (SILU) {
+      const int tt = row >> 4, rr = row & 15;
+      const int idx = bn * 64 + (tt >> 1) * 16 + rr;
+      wsrc[i] = static_cast<const bf16_t*>(a.W.ptr[tt & 1]) + static_cast<size_t>(idx) * K + col;
+    } else {
+      wsrc[i] = seg_row<bf16_t>(a.W, bn * kTBN + row, K) + col;
+    }
+    int m = bm * kTBM + row;
+    if (m >= a.M) m = a.M - 1;
+    asrc[i] = static_cast<const bf16_t*>(a.A) + static_cast<size_t>(m) * a.lda + col;
+    lds_off[i] = row * kTLDK + col;
+  }
+
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[t][u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int kb0 = split * kblocks_per_split;
+  const int kb1 = min(kb0 + kblocks_per_split, K / kTBK);
+  uint4 wreg[4], areg[4];
+  if (kb0 < kb1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      wreg[i] = *reinterpret_cast<const uint4*>(wsrc[i] + kb0 * kTBK);
+      areg[i] = *reinterpret_cast<const uint4*>(asrc[i] + kb0 * kTBK);
+    }
+  }
+  for (int kb = kb0; kb < kb1; ++kb) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<uint4*>(&Ws[lds_off[i]]) = wreg[i];
+      *reinterpret_cast<uint4*>(&As[lds_off[i]]) = areg[i];
+    }
+    __syncthreads();
+    if (kb + 1 < kb1) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        wreg[i] = *reinterpret_cast<const uint4*>(wsrc[i] + (kb + 1) * kTBK);
+        areg[i] = *reinterpret_cast<const uint4*>(asrc[i] + (kb + 1) * kTBK);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < kTBK; kk += 32) {
+      bf16x8_t af[4], bfr[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) af[t] = load_bf16x8(&Ws[(wn * 64 + t * 16 + r) * kTLDK + kk + g * 8]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) bfr[u] = load_bf16x8(&As[(wm * 64 + u * 16 + r) * kTLDK + kk + g * 8]);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[t][u] = mfma16x16x32(af[t], bfr[u], acc[t][u]);
+    }
+  }
+
+  // lane (g, c) holds C^T[n = wn*64 + t*16 + 4g + e][m = wm*64 + u*16 + c]
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int m = bm * kTBM + wm * 64 + u * 16 + r;
+    if (m >= a.M) continue;
+    if (SILU) {
+      bf16_t* out = static_cast<bf16_t*>(a.act_out);
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const int i0 = bn * 64 + (wn * 2 + p) * 16 + g * 4;
+        uint2 pk;
+        pk.x = static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][0]) * acc[2 * p + 1][u][0])) |
+               (static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][1]) * acc[2 * p + 1][u][1])) << 16);
+        pk.y = static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][2]) * acc[2 * p + 1][u][2])) |
+               (static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][3]) * acc[2 * p + 1][u][3])) << 16);
+        *reinterpret_cast<uint2*>(out + static_cast<size_t>(m) * a.N + i0) = pk;
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int n = bn * kTBN + wn * 64 + t * 16 + g * 4;
+        float4 v = make_float4(acc[t][u][0], acc[t][u][1], acc[t][u][2], acc[t][u][3]);
+        *reinterpret_cast<float4*>(a.part + (static_cast<size_t>(split) * a.M + m) * a.N + n) = v;
+      }
+    }
+  }
+}
+
+// ---- fp32 model ------------------------------------------------------------
+template <bool SILU>
+__global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs a) {
+  constexpr int BM = 64, BN = 64, BK = 16;
+  constexpr int NW = SILU ? 2 : 1;
+  __shared__ float As[BK][BM + 1];
+  __shared__ float Ws[NW][BK][BN + 1];
+  const int tid = threadIdx.x;
+  const int tx = tid & 15, ty = tid >> 4;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const float* A = static_cast<const float*>(a.A);
+  float acc[NW][4][4];
+#pragma unroll
+  for (int w = 0; w < NW; ++w)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[w][i][j] = 0.f;
+
+  for (int k0 = 0; k0 < a.K; k0 += BK) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = tid + 256 * i;
+      const int row = e >> 4, kk = e & 15;
+      const int m = m0 + row, k = k0 + kk, n = n0 + row;
+      As[kk][row] = (m < a.M && k < a.K) ? A[static_cast<size_t>(m) * a.lda + k] : 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        float v = 0.f;
+        if (n < a.N && k < a.K) {
+          const float* wr = SILU ? static_cast<const float*>(a.W.ptr[w]) + static_cast<size_t>(n) * a.K
+                                 : seg_row<float>(a.W, n, a.K);
+          v = wr[k];
+        }
+        Ws[w][kk][row] = v;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < BK; ++kk) {
+      float av[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float wv = Ws[w][kk][tx * 4 + j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[w][i][j] = fmaf(av[i], wv, acc[w][i][j]);
+        }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= a.M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx * 4 + j;
+      if (n >= a.N) continue;
+      if (SILU) static_cast<float*>(a.act_out)[static_cast<size_t>(m) * a.N + n] = silu(acc[0][i][j]) * acc[NW - 1][i][j];
+      else a.part[static_cast<size_t>(m) * a.N + n] = acc[0][i][j];
+    }
+  }
+}
+
+template <int R, int MT, bool SILU>
+void launch_stream_t(const GemmArgs& a, hipStream_t s) {
+  const int n_chunks = a.K / 128;
+  const int cps = (n_chunks + a.splits - 1) / a.splits;
+  const int blocks = SILU ? a.N / 16 : a.N / (16 * R);
+  hipLaunchKernelGGL((k_gemm_stream<R, MT, SILU>), dim3(blocks, a.splits), dim3(256), 0, s, a, cps);
+}
+
+template <bool SILU>
+void launch_stream_m(const GemmArgs& a, hipStream_t s) {
+  const int mt = (a.M + 15) / 16;
+  switch (mt) {
+    case 1: launch_stream_t<2, 1, SILU>(a, s); break;
+    case 2: launch_stream_t<2, 2, SILU>(a, s); break;
+    case 3: launch_stream_t<2, 3, SILU>(a, s); break;
+    default: launch_stream_t<2, 4, SILU>(a, s); break;
+  }
+}
+
+}  // namespace
+
+int gemm_pick_splits(int bf16, int M, int N, int K, int max_splits) {
+  if (!bf16) return 1;
+  int blocks, max_by_k;
+  if (M <= 64) {
+    blocks = N / 32;
+    max_by_k = (K / 128) / 4;  // at least one chunk per wave
+  } else {
+    blocks = (N / kTBN) * ((M + kTBM - 1) / kTBM);
+    max_by_k = (K / kTBK) / 4;
+  }
+  int s = (512 + blocks - 1) / blocks;
+  if (s > max_by_k) s = max_by_k;
+  if (s > max_splits) s = max_splits;
+  return s < 1 ? 1 : s;
+}
+
+hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.splits < 1 || (a.epi == kEpiSiluMul && a.splits != 1)) return hipErrorInvalidValue;
+  if (!bf16) {
+    if (a.splits != 1) return hipErrorInvalidValue;
+    dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
+    if (a.epi == kEpiSiluMul) hipLaunchKernelGGL(k_gemm_f32<true>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_gemm_f32<false>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.M <= 64) {
+    if (a.K % 128 != 0 || a.N % (a.epi == kEpiSiluMul ? 16 : 32) != 0) return hipErrorInvalidValue;
+    if (a.epi == kEpiSiluMul) launch_stream_m<true>(a, s);
+    else launch_stream_m<false>(a, s);
+  } else {
+    if (a.K % kTBK != 0 || a.N % (a.epi == kEpiSiluMul ? 64 : kTBN) != 0) return hipErrorInvalidValue;
+    const int kbps = (a.K / kTBK + a.splits - 1) / a.splits;
+    const int nb = a.epi == kEpiSiluMul ? a.N / 64 : a.N / kTBN;
+    dim3 grid(nb, (a.M + kTBM - 1) / kTBM, a.splits);
+    if (a.epi == kEpiSiluMul) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps);
+    else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(256), 0, s, a, kbps);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace rollpack

@@ -1,0 +1,114 @@
+// Kernel launchers of the rollout path (host-callable, gfx950 device code).
+//
+// Data layout in HBM (all row-major):
+//   x      fp32 [M, H]               residual stream
+//   h      T    [M, H]               normalised GEMM input (T = float or bf16)
+//   part   fp32 [S, M, N]            split-K partial GEMM outputs, summed by the consumer
+//   q      T    [M, n_q, hd]         rotated queries
+//   K pool T    [layer][page][n_kv][64 tokens][hd]
+//   V pool T    [layer][page][n_kv][hd][64 tokens]   (transposed per page)
+//   page table int32 [slot][max_pages_per_seq]
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rollpack {
+
+constexpr int kPageTokens = 64;
+
+// Weight rows split over up to three tensors (q/k/v, or gate/up).  Each
+// segment holds `rows` rows of K elements; rows are multiples of 16.
+struct WSeg {
+  const void* ptr[3];
+  int32_t rows[3];
+  int32_t n_seg;
+};
+
+enum GemmEpilogue { kEpiPartial = 0, kEpiSiluMul = 1 };
+
+struct GemmArgs {
+  const void* A;     // [M, lda] activations (dtype T)
+  int64_t lda;
+  int M, N, K;       // N: output columns (for kEpiSiluMul: I, with W = {gate, up})
+  WSeg W;
+  int epi;
+  int splits;        // S >= 1; kEpiSiluMul requires 1
+  float* part;       // [S, M, N] (kEpiPartial)
+  void* act_out;     // [M, N] dtype T (kEpiSiluMul)
+};
+
+// Picks the kernel from dtype and M.  Returns hipSuccess or a launch error.
+hipError_t launch_gemm(int dtype_bf16, const GemmArgs& a, hipStream_t s);
+// Split count the launcher would like for this shape (1 = none).
+int gemm_pick_splits(int dtype_bf16, int M, int N, int K, int max_splits);
+
+struct EmbedArgs {
+  const void* embed; const void* norm_g;
+  const int32_t* in_tok;     // [M]; < 0: take tokens_cur[row_slot[i]]
+  const int32_t* row_slot;   // [M] (only read when in_tok < 0)
+  const int32_t* tokens_cur; // [slots]
+  int M, H; float eps;
+  float* x; void* h;
+};
+hipError_t launch_embed_norm(int bf16, const EmbedArgs& a, hipStream_t s);
+
+struct AddNormArgs {
+  float* x; const float* part; int splits;   // x += sum_s part[s] (part may be null)
+  const void* norm_g; int M, H; float eps;
+  void* h;
+};
+hipError_t launch_add_rmsnorm(int bf16, const AddNormArgs& a, hipStream_t s);
+
+struct RopeArgs {
+  const float* part; int splits; int M;          // part [S, M, Nqkv]
+  const void* bq; const void* bk; const void* bv;
+  int n_q, n_kv, hd;
+  const int32_t* pos; const int32_t* slot;       // [M]
+  const int32_t* page_table; int32_t pt_stride;
+  const float* rope_cos; const float* rope_sin;  // [max_ctx, hd/2]
+  void* q_out;                                   // [M, n_q, hd]
+  void* k_pool; void* v_pool;                    // this layer's pools
+};
+hipError_t launch_rope_append(int bf16, const RopeArgs& a, hipStream_t s);
+
+struct AttnArgs {
+  const void* q;                  // [rows, n_q, hd]
+  const void* k_pool; const void* v_pool;
+  const int32_t* page_table; int32_t pt_stride;
+  int n_q, n_kv, hd;
+  float scale;                    // 1 / sqrt(hd)
+  // fp32 model: one query row per (token, head), keys 0..tok_pos[row]
+  int n_rows; const int32_t* tok_slot; const int32_t* tok_pos;
+  // decode (one query token per sequence, split over the context):
+  int B; const int32_t* row_slot; const int32_t* row_ctx; const int32_t* split_off;
+  int total_splits; int tokens_per_split;
+  float* part_o; float* part_ml;  // [total_splits * n_kv, 16, hd], [.., 2, 16]
+  // prefill (causal over packed prompt chunks):
+  int n_seq; const int32_t* seq_slot; const int32_t* seq_row0; const int32_t* seq_pos0;
+  const int32_t* seq_ntok; const int32_t* item_off; int total_items;
+  // output [rows, n_q * hd]
+  void* out;
+};
+hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_prefill(int bf16, const AttnArgs& a, hipStream_t s);
+// Combine decode splits into out (bf16 model only).
+hipError_t launch_attn_merge(const AttnArgs& a, hipStream_t s);
+// Query tokens per prefill work item for a GQA group size.
+int attn_prefill_tokens_per_item(int bf16, int group);
+
+struct SampleArgs {
+  const float* logits; int B; int V;
+  const int32_t* row_slot;        // [B]
+  const int32_t* row_pos;         // [B] absolute position of the token being sampled
+  const int32_t* row_hist;        // [B] index into the slot's token history
+  const uint64_t* slot_seed; const uint64_t* slot_id; const float* slot_temp;
+  int32_t* tokens_cur; int32_t* hist; int64_t hist_stride;
+};
+hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
+
+// out[i, :] = src[rows[i], :] for i < n (element size esize bytes, H elements)
+hipError_t launch_gather_rows(const void* src, const int32_t* rows, int n, int H, int esize,
+                              void* out, hipStream_t s);
+
+}  // namespace rollpack

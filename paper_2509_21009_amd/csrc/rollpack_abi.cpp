@@ -1,0 +1,186 @@
+// extern "C" surface of the rollout library (declared in include/rollpack.h).
+// Every entry point validates its arguments, converts exceptions into
+// rp_status codes and records a thread-local message for rp_last_error().
+#include <cmath>
+#include <new>
+#include <string>
+
+#include "engine.hpp"
+#include "tail_batch.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+template <typename F>
+rp_status guarded(F&& f) {
+  try {
+    f();
+    g_last_error.clear();
+    return RP_OK;
+  } catch (const rollpack::RpError& e) {
+    g_last_error = e.what();
+    return e.status;
+  } catch (const std::bad_alloc&) {
+    g_last_error = "host allocation failed";
+    return RP_ERR_CAPACITY;
+  } catch (const std::exception& e) {
+    g_last_error = e.what();
+    return RP_ERR_INVALID_ARG;
+  }
+}
+
+rollpack::Engine* live_engine(rp_engine* eng) {
+  if (!eng || !eng->impl) throw rollpack::RpError(RP_ERR_INVALID_ARG, "null engine");
+  if (eng->impl->broken())
+    throw rollpack::RpError(RP_ERR_BAD_STATE, "engine is unusable after an earlier HIP error");
+  return eng->impl;
+}
+
+// Marks the engine unusable when a HIP error escapes mid-operation.
+template <typename F>
+rp_status engine_call(rp_engine* eng, F&& f) {
+  return guarded([&] {
+    rollpack::Engine* e = live_engine(eng);
+    try {
+      f(e);
+    } catch (const rollpack::RpError& err) {
+      if (err.status == RP_ERR_HIP) e->mark_broken();
+      throw;
+    }
+  });
+}
+
+}  // namespace
+
+extern "C" {
+
+rp_status rp_kv_bytes_per_token(const rp_model_config* cfg, size_t* bytes) {
+  return guarded([&] {
+    if (!cfg || !bytes) throw rollpack::RpError(RP_ERR_INVALID_ARG, "null argument");
+    rollpack::validate_config(*cfg);
+    const size_t esz = cfg->dtype == RP_DTYPE_BF16 ? 2 : 4;
+    *bytes = static_cast<size_t>(cfg->n_layers) * 2 * cfg->n_kv_heads * cfg->head_dim * esz;
+  });
+}
+
+rp_status rp_workspace_size(const rp_model_config* cfg, const rp_engine_limits* limits, size_t* kv_bytes,
+                            size_t* scratch_bytes) {
+  return guarded([&] {
+    if (!cfg || !limits || !kv_bytes || !scratch_bytes) throw rollpack::RpError(RP_ERR_INVALID_ARG, "null argument");
+    rollpack::validate_config(*cfg);
+    rollpack::validate_limits(*limits);
+    *kv_bytes = rollpack::kv_pool_bytes(*cfg, limits->kv_pages);
+    *scratch_bytes = rollpack::plan_scratch(*cfg, *limits).total;
+  });
+}
+
+rp_status rp_engine_create(const rp_model_config* cfg, const rp_weights* weights, const rp_engine_limits* limits,
+                           void* kv_ws, size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, void* hip_stream,
+                           rp_engine** out) {
+  return guarded([&] {
+    if (!cfg || !weights || !limits || !out) throw rollpack::RpError(RP_ERR_INVALID_ARG, "null argument");
+    *out = nullptr;
+    rollpack::validate_config(*cfg);
+    rollpack::validate_limits(*limits);
+    auto* impl = new rollpack::Engine(*cfg, *weights, *limits, kv_ws, kv_bytes, scratch_ws, scratch_bytes,
+                                      static_cast<hipStream_t>(hip_stream));
+    *out = new rp_engine{impl};
+  });
+}
+
+void rp_engine_destroy(rp_engine* eng) {
+  if (!eng) return;
+  delete eng->impl;
+  delete eng;
+}
+
+rp_status rp_prefill(rp_engine* eng, int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
+                     const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed, float temperature,
+                     float* logits_out, int32_t* first_tokens_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    e->prefill(n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature, logits_out,
+               first_tokens_out);
+  });
+}
+
+rp_status rp_decode_step(rp_engine* eng, const int32_t* forced_tokens, float* logits_out, int64_t* row_ids_out,
+                         int32_t* n_active_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    const int32_t b = e->decode_step(forced_tokens, logits_out, row_ids_out);
+    if (n_active_out) *n_active_out = b;
+  });
+}
+
+rp_status rp_free_finished(rp_engine* eng, int64_t* finished_ids_out, int32_t cap, int32_t* n_finished_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    if (cap < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "cap must be >= 0");
+    const int32_t k = e->free_finished(finished_ids_out, cap);
+    if (n_finished_out) *n_finished_out = k;
+  });
+}
+
+rp_status rp_abort(rp_engine* eng, int32_t n, const int64_t* seq_ids) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->abort(n, seq_ids); });
+}
+
+rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t cap, int32_t* len_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    if (cap < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "cap must be >= 0");
+    const int32_t k = e->get_tokens(seq_id, out, cap);
+    if (len_out) *len_out = k;
+  });
+}
+
+rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
+                              const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed,
+                              float temperature, const int32_t* round_ids, int32_t* resp_tokens_out,
+                              rp_round_stats* stats_out, int32_t max_stats, int32_t* n_rounds_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    const int32_t r = e->rollout(n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
+                                 round_ids, resp_tokens_out, stats_out, max_stats);
+    if (n_rounds_out) *n_rounds_out = r;
+  });
+}
+
+rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens, int32_t P0, int32_t R0,
+                                float eta, int32_t max_rounds, int32_t cap_launch, int32_t* round_kind_out,
+                                int32_t* round_time_out, int32_t* launch_off_out, int32_t* launch_prompt_out,
+                                int32_t* run_steps_out, int32_t* accept_round_out, int32_t* kept_out,
+                                int32_t* n_rounds_out) {
+  return guarded([&] {
+    if (n_prompts < 0 || r_spec < 1 || (n_prompts > 0 && !lens) || !n_rounds_out || max_rounds < 0 ||
+        cap_launch < 0)
+      throw rollpack::RpError(RP_ERR_INVALID_ARG, "tail batching: bad arguments");
+    for (int64_t i = 0; i < static_cast<int64_t>(n_prompts) * r_spec; ++i)
+      if (lens[i] < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "tail batching: negative length");
+    const rollpack::TailBatchPlan plan = rollpack::plan_tail_batching(n_prompts, r_spec, lens, P0, R0, eta);
+    const int32_t nr = static_cast<int32_t>(plan.rounds.size());
+    size_t launches = 0;
+    for (const auto& r : plan.rounds) launches += r.launched.size();
+    if (nr > max_rounds || launches > static_cast<size_t>(cap_launch))
+      throw rollpack::RpError(RP_ERR_CAPACITY, "tail batching: output arrays too small");
+    if (!round_kind_out || !round_time_out || !launch_off_out || !launch_prompt_out || !run_steps_out ||
+        !accept_round_out || !kept_out)
+      throw rollpack::RpError(RP_ERR_INVALID_ARG, "tail batching: null output array");
+    size_t pos = 0;
+    launch_off_out[0] = 0;
+    for (int32_t k = 0; k < nr; ++k) {
+      const auto& r = plan.rounds[k];
+      round_kind_out[k] = r.kind;
+      round_time_out[k] = r.time;
+      for (size_t j = 0; j < r.launched.size(); ++j, ++pos) {
+        launch_prompt_out[pos] = r.launched[j];
+        for (int32_t q = 0; q < r_spec; ++q) run_steps_out[pos * r_spec + q] = r.run_steps[j * r_spec + q];
+      }
+      launch_off_out[k + 1] = static_cast<int32_t>(pos);
+    }
+    for (int32_t p = 0; p < n_prompts; ++p) accept_round_out[p] = plan.accept_round[p];
+    for (size_t i = 0; i < plan.kept.size(); ++i) kept_out[i] = plan.kept[i];
+    *n_rounds_out = nr;
+  });
+}
+
+const char* rp_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

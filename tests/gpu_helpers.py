@@ -1,0 +1,90 @@
+"""Shared helpers of the GPU parity tests (imported by tests marked gpu)."""
+from __future__ import annotations
+
+import dataclasses
+import os
+import sys
+
+import numpy as np
+
+from oracle import model as om
+from oracle import sampling as osm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def log(msg: str):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def rp():
+    from paper_2509_21009_amd import rollpack
+    if not os.path.exists(rollpack.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    rollpack.load_library()
+    return rollpack
+
+
+def to_device(w: dict, dev) -> dict:
+    return {"embed": w["embed"].to(dev), "final_norm": w["final_norm"].to(dev),
+            "lm_head": None if w["lm_head"] is None else w["lm_head"].to(dev),
+            "layers": [{k: v.to(dev).contiguous() for k, v in L.items()} for L in w["layers"]]}
+
+
+@dataclasses.dataclass
+class ParityResult:
+    max_rel_err: float
+    positions: int
+    greedy_agree: int
+    id_checked: int
+    id_mismatch: int
+    worst: tuple
+
+
+def oracle_rollout(w64, shape, prompt, n_new, temperature, seed, seq_id):
+    sample_fn = osm.sampler(temperature, seed, seq_id)
+    return om.generate(w64, shape, prompt, n_new, sample_fn)
+
+
+def teacher_forced_parity(eng, shape, w64, wl, n_new, tol, temperature, seed):
+    """Prefill + (n_new - 1) teacher-forced decode steps on the GPU vs the oracle.
+
+    Per position r: e_r = max|l_gpu - l_ref| / max|l_ref|; the GPU's sampled
+    id must equal the oracle's wherever the oracle's top-2 score gap exceeds
+    tol * max|l_ref| / T (T = 1 for greedy).
+    """
+    import torch
+    n = wl.n
+    refs = [oracle_rollout(w64, shape, wl.prompt(i), n_new, temperature, seed, int(wl.seq_ids[i]))
+            for i in range(n)]
+    ref_tok = np.stack([r[0] for r in refs])          # [n, n_new]
+    ref_log = np.stack([r[1] for r in refs])          # [n, n_new, V]
+    max_new = np.full(n, n_new, np.int32)
+    logits0, _ = eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, max_new, seed, temperature,
+                             logits=True)
+    gpu_log = [logits0.cpu().numpy().astype(np.float64)]
+    for j in range(1, n_new):
+        b, rows, lg = eng.decode_step(forced_tokens=ref_tok[:, j - 1], logits=True)
+        assert b == n and np.array_equal(rows, wl.seq_ids)
+        gpu_log.append(lg.cpu().numpy().astype(np.float64))
+    torch.cuda.synchronize()
+    gpu_log = np.stack(gpu_log, axis=1)               # [n, n_new, V]
+    gpu_tok = np.stack([eng.get_tokens(int(i), n_new) for i in wl.seq_ids])
+    freed = eng.free_finished()
+    assert sorted(freed.tolist()) == sorted(wl.seq_ids.tolist())
+    err = np.max(np.abs(gpu_log - ref_log), axis=-1) / np.max(np.abs(ref_log), axis=-1)
+    agree = int(np.sum(np.argmax(gpu_log, -1) == np.argmax(ref_log, -1)))
+    checked = mism = 0
+    t_eff = temperature if temperature > 0 else 1.0
+    for i in range(n):
+        for j in range(n_new):
+            pos = len(wl.prompt(i)) + j
+            s = osm.scores(ref_log[i, j], temperature, seed, int(wl.seq_ids[i]), pos)
+            tau = tol * np.max(np.abs(ref_log[i, j])) / t_eff
+            if osm.top2_gap(s) > tau:
+                checked += 1
+                if gpu_tok[i, j] != ref_tok[i, j]:
+                    mism += 1
+    worst = np.unravel_index(np.argmax(err), err.shape)
+    return ParityResult(float(err.max()), int(err.size), agree, checked, mism, tuple(int(v) for v in worst))

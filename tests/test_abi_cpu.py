@@ -1,0 +1,149 @@
+"""CPU checks of the C-ABI library: it loads, exports every declared symbol,
+its host-only calls behave, and the host C++ passes its sanitizer build."""
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle import schedule as osch
+from paper_2509_21009_amd import rollpack as rp
+from workloads import SHAPES, make_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rollpack.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rp.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return rp.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rp_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("rp_prefill", "rp_decode_step", "rp_free_finished", "rp_rollout_generate",
+                     "rp_engine_create", "rp_workspace_size", "rp_plan_tail_batching", "rp_last_error"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+    out = subprocess.run(["nm", "-D", "--defined-only", rp.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (rp_\w+)", out))
+    assert set(declared_functions()) <= exported
+    assert set(rp.SIGNATURES) == set(declared_functions())
+
+
+def test_workspace_size_and_kv_bytes(lib):
+    s = SHAPES["qwen2.5-7b"]
+    cfg = rp.model_config(s)
+    assert rp.rp_kv_bytes_per_token(cfg) == s.kv_bytes_per_token() == 57344
+    lim = rp.RpEngineLimits(64, 4096, 17408, 64, 1000)
+    kv, sc = rp.rp_workspace_size(cfg, lim)
+    assert kv == 1000 * 64 * 57344 and kv % 256 == 0 and sc % 256 == 0 and sc > 0
+    lim2 = rp.RpEngineLimits(64, 4096, 17408, 64, 2000)
+    assert rp.rp_workspace_size(cfg, lim2)[0] == 2 * kv
+
+
+@pytest.mark.parametrize("field,value", [("head_dim", 96), ("n_kv_heads", 3), ("hidden", 100), ("vocab", 1000)])
+def test_invalid_configs_are_rejected(lib, field, value):
+    import dataclasses
+    cfg = rp.model_config(dataclasses.replace(SHAPES["qwen2.5-0.5b"], **{
+        {"head_dim": "head_dim", "n_kv_heads": "n_kv", "hidden": "hidden", "vocab": "vocab"}[field]: value}))
+    with pytest.raises(rp.RollpackError) as e:
+        rp.rp_workspace_size(cfg, rp.RpEngineLimits(8, 128, 256, 64, 16))
+    assert e.value.status == 1 and rp.rp_last_error()
+
+
+@pytest.mark.parametrize("lim", [(0, 128, 256, 64, 16), (8, 128, 256, 32, 16), (8, 128, 1, 64, 16),
+                                 (8, 128, 256, 64, 0), (8, 128, 70000, 64, 16)])
+def test_invalid_limits_are_rejected(lib, lim):
+    with pytest.raises(rp.RollpackError) as e:
+        rp.rp_workspace_size(rp.model_config(SHAPES["tiny"]), rp.RpEngineLimits(*lim))
+    assert e.value.status == 1
+
+
+def test_engine_create_rejects_bad_workspaces_without_gpu(lib):
+    s = SHAPES["tiny"]
+    cfg = rp.model_config(s)
+    lim = rp.RpEngineLimits(4, 64, 128, 64, 8)
+    layers = (rp.RpLayerWeights * s.layers)()
+    w = rp.RpWeights(None, None, None, layers)
+    with pytest.raises(rp.RollpackError) as e:
+        rp.rp_engine_create(cfg, w, lim, 0, 0, 0, 0, 0)
+    assert e.value.status == 1
+
+
+def test_null_engine_calls_fail_cleanly(lib):
+    n = rp.ctypes.c_int32()
+    assert lib.rp_decode_step(None, None, None, None, rp.ctypes.byref(n)) == 1
+    assert "null engine" in rp.rp_last_error()
+
+
+def _lens(seed, n, r_spec):
+    rng = np.random.default_rng(seed)
+    return np.clip(np.rint(300 * np.exp(0.9 * rng.standard_normal((n, r_spec)))), 1, 8000).astype(np.int32)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_tail_batching_plan_matches_oracle(lib, seed):
+    rng = np.random.default_rng(seed)
+    P0, R0 = int(rng.integers(1, 9)), int(rng.integers(1, 9))
+    eta = float(rng.choice([1.0, 1.25, 1.5]))
+    r_spec = math.ceil(eta * R0)
+    n = int(rng.integers(0, 60))
+    lens = _lens(seed, n, r_spec)
+    ours, acc, kept = rp.rp_plan_tail_batching(lens.reshape(n, r_spec), P0, R0, eta)
+    ref = osch.plan_tail_batching(lens.tolist(), P0, R0, eta)
+    assert len(ours) == len(ref)
+    for a, b in zip(ours, ref):
+        assert a["kind"] == b["kind"] and a["time"] == b["time"]
+        assert a["launched"] == sorted(b["launched"])
+        for (p, r), t in a["run"].items():
+            assert t == b["run"].get((p, r), 0)
+    for k, b in enumerate(ref):
+        for p in b["accepted"]:
+            assert acc[p] == k
+            assert sorted(np.flatnonzero(kept[p]).tolist()) == b["kept"][p]
+
+
+def test_tail_batching_rejects_bad_arguments(lib):
+    with pytest.raises(rp.RollpackError):
+        rp.rp_plan_tail_batching(np.ones((3, 2), np.int32), 0, 2, 1.0)
+    with pytest.raises(rp.RollpackError):
+        rp.rp_plan_tail_batching(np.ones((3, 2), np.int32), 1, 2, 1.25)   # r_spec must be ceil(1.25*2)=3
+
+
+def test_host_cpp_under_sanitizers(tmp_path):
+    csrc = os.path.join(ROOT, "paper_2509_21009_amd", "csrc")
+    exe = tmp_path / "test_host"
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           f"-I{csrc}", os.path.join(ROOT, "tests", "cpp", "test_host.cpp"), os.path.join(csrc, "tail_batch.cpp"),
+           "-o", str(exe)]
+    subprocess.run(cmd, check=True, capture_output=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, env={**os.environ, "ASAN_OPTIONS": "detect_leaks=1"})
+    assert r.returncode == 0, r.stderr
+    assert "host tests passed" in r.stdout
+
+
+def test_workload_shapes_follow_the_configs():
+    w = make_workload("7b-long")
+    assert w.n == 64 and w.max_new.min() >= 512 and w.max_new.max() <= 16384
+    pl = w.prompt_lens()
+    assert pl.min() >= 128 and pl.max() <= 1024
+    m = make_workload("7b-mixed")
+    assert m.n == 576 and set(m.round_id.tolist()) == {0, 1} and len(set(m.seq_ids.tolist())) == 576
+    c2 = make_workload("0.5b")
+    assert c2.n == 256 and len(set(c2.prompt_group.tolist())) == 32
