@@ -1,0 +1,218 @@
+#!/usr/bin/env python3
+"""Rollout benchmark on one MI355X.
+
+One "step" is one whole rollout round of the workload through the C ABI
+(rp_rollout_generate): round formation, paged-KV admission, chunked prefill,
+decode steps until the longest response is done with finished sequences
+freed as they go, seeded sampling and round metrics.  Inputs (weights,
+prompts) are resident in HBM / host memory before the timed region.
+
+Default workload: Qwen2.5-7B shape, bf16 random weights, the long round of 64
+sequences with long-tail forced response lengths (lognormal, median 4096,
+sigma 1.0, clamped to [512, 16384]), temperature 1.0.
+
+Prints one JSON line.  `--gpus N` with N > 1 is refused: this build runs on
+a single GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/s/GPU + % peak HBM BW, Qwen2.5-7B-shape long-tail rollout"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+WORKLOAD_TEXT = {
+    "7b-long": "Qwen2.5-7B shape long round: 64 seqs, prompts U[128,1024], responses LogN(4096, 1.0) "
+               "clamped [512,16384], forced lengths, T=1.0",
+    "7b-short": "Qwen2.5-7B shape short round: 512 seqs, prompts U[128,1024], responses LogN(768, 0.4) "
+                "clamped [64,2048], T=1.0",
+    "7b-mixed": "Qwen2.5-7B shape: short round (512 seqs) then long round (64 seqs), given round ids",
+    "0.5b": "Qwen2.5-0.5B shape: 32 prompts x 8 responses, prompts U[64,512], LogN(512, 0.8) clamped "
+            "[32,4096], T=1.0",
+    "32b": "Qwen2.5-32B shape: 96 seqs, prompts U[256,1024], LogN(2048, 0.9) clamped [64,8192], T=1.0",
+    "tiny": "tiny fp32 decoder: 8 prompts x 32 tokens, 64 greedy tokens each",
+}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def decode_bytes_model(shape, prompt_lens, max_new):
+    """Algorithmic HBM bytes of every decode step of one round: the weights
+    once per step plus the K/V of every attended token."""
+    wbytes = shape.decode_weight_bytes()
+    kvb = shape.kv_bytes_per_token()
+    p = np.asarray(prompt_lens, np.int64)
+    L = np.asarray(max_new, np.int64)
+    steps = int(L.max()) - 1
+    total = 0.0
+    for j in range(1, steps + 1):
+        act = L > j
+        total += wbytes + float(np.sum(p[act] + j)) * kvb
+    return total, steps
+
+
+def cpu_baseline(weights, shape, wl):
+    """Time the oracle on a bounded sample and scale it to generated tokens/s.
+
+    Sample: one sequence of the workload (its real prompt), the first layer
+    plus the LM head, prefill then 4 decode steps; the per-layer share of the
+    times is scaled to all layers.  The oracle decodes one sequence at a time,
+    so its rate over the workload is sum(L) / sum(prefill_i + L_i * step).
+    """
+    from threadpoolctl import threadpool_info
+
+    from oracle import model as om
+    from workloads import truncated, weights_to_numpy
+
+    sub = {"embed": weights["embed"], "final_norm": weights["final_norm"], "lm_head": weights["lm_head"],
+           "layers": weights["layers"][:1]}
+    w64 = weights_to_numpy(sub)
+    s1 = truncated(shape, 1)
+    prompt = wl.prompt(0)
+    st = om.KVState(s1)
+    t0 = time.perf_counter()
+    logits = st.step(w64, prompt)[-1]
+    t_prefill_1 = time.perf_counter() - t0
+    tok = int(np.argmax(logits))
+    times = []
+    for _ in range(4):
+        t0 = time.perf_counter()
+        tok = int(np.argmax(st.step(w64, [tok])[-1]))
+        times.append(time.perf_counter() - t0)
+    t_dec_1 = float(np.median(times))
+    x = np.random.default_rng(0).standard_normal((1, shape.hidden))
+    lm = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        om.lm_head(w64, x, s1)
+        lm.append(time.perf_counter() - t0)
+    t_lm = float(np.median(lm))
+    t_step = shape.layers * max(t_dec_1 - t_lm, 0.0) + t_lm
+    t_pre_per_tok = shape.layers * max(t_prefill_1 - t_lm, 0.0) / len(prompt)
+    plens = wl.prompt_lens()
+    total_t = float(np.sum(plens * t_pre_per_tok + t_lm + (wl.max_new - 1) * t_step))
+    rate = float(np.sum(wl.max_new)) / total_t
+    threads = sum(int(i.get("num_threads", 0)) for i in threadpool_info() if i.get("user_api") == "blas") or 1
+    return {"value": rate, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"fp64 numpy oracle, sequence 0 of the workload (prompt {len(prompt)} tokens): prefill and "
+                       f"4 decode steps through layer 0 + LM head, per-layer time x{shape.layers} layers, "
+                       f"extrapolated over all {wl.n} sequences ({int(np.sum(wl.max_new))} tokens); "
+                       f"measured step {t_step:.2f} s/token, host cpus {len(os.sched_getaffinity(0))}"),
+            "extrapolated": True}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="7b-long", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--kernel", default="gemm_gate_up", help="kernel class whose roofline is reported")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--max-prefill-tokens", type=int, default=16384)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "rollout sequences shard across GPUs as independent engines, which this build does not run.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2509_21009_amd import rollpack as rp
+    from workloads import make_weights, make_workload
+
+    if not os.path.exists(rp.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    rp.load_library()
+    dev = torch.device("cuda:0")
+    wl = make_workload(args.workload)
+    shape = wl.shape
+    log(f"workload {args.workload}: {wl.n} seqs, {int(wl.max_new.sum())} new tokens, max {int(wl.max_new.max())}")
+    t0 = time.perf_counter()
+    weights = make_weights(shape, seed=0, device=dev)
+    torch.cuda.synchronize()
+    log(f"weights generated in {time.perf_counter() - t0:.1f} s")
+    wd = rp.weights_for_engine(weights)
+    plens = wl.prompt_lens()
+    need_ctx = int(np.max(plens + wl.max_new))
+    pages = int(np.sum((plens + wl.max_new - 1 + 63) // 64)) + 16
+    eng = rp.Engine(shape, wd, max_seqs=wl.n, max_prefill_tokens=max(args.max_prefill_tokens, int(plens.max())),
+                    max_context=need_ctx, kv_pages=pages)
+    call = lambda: eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, wl.sample_seed,  # noqa
+                               wl.temperature, wl.round_id)
+    for i in range(args.warmup):
+        t0 = time.perf_counter()
+        call()
+        log(f"warmup step {i + 1}/{args.warmup} done in {time.perf_counter() - t0:.1f} s")
+    eng.profile([args.kernel])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    all_stats = []
+    for i in range(args.steps):
+        _, stats = call()
+        all_stats.append(stats)
+        log(f"timed step {i + 1}/{args.steps}: " + ", ".join(
+            f"round {s['round_id']}: {s['makespan_ms'] / 1e3:.2f} s" for s in stats))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = eng.profile_read()
+    eng.profile([])
+
+    gen_tokens = int(wl.max_new.sum()) * args.steps
+    value = gen_tokens / elapsed
+    last = all_stats[-1]
+    decode_s = sum(s["decode_ms"] for s in last) / 1e3
+    makespan_s = sum(s["makespan_ms"] for s in last) / 1e3
+    dec_bytes = 0.0
+    rounds = [np.arange(wl.n)] if wl.round_id is None else [np.flatnonzero(wl.round_id == r)
+                                                             for r in sorted(set(wl.round_id.tolist()))]
+    for idx in rounds:
+        b, _ = decode_bytes_model(shape, plens[idx], wl.max_new[idx])
+        dec_bytes += b
+    dec = [p for p in prof if p["phase"] == "decode" and p["kernel"] == args.kernel]
+    roof = None
+    if dec:
+        p = dec[0]
+        avg_ms = p["total_ms"] / p["launches"]
+        bytes_per = p["bytes"] / p["launches"]
+        achieved = bytes_per / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": args.kernel,
+                "phase": "decode", "launches": p["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
+                "algorithmic_bytes_per_launch": bytes_per}
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 1), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "sequences": wl.n,
+                   "generated_tokens_per_step": int(wl.max_new.sum()),
+                   "prompt_tokens_per_step": int(plens.sum()),
+                   "makespan_s": round(makespan_s, 3), "decode_s": round(decode_s, 3),
+                   "decode_tokens_per_s": round(int(wl.max_new.sum()) / max(decode_s, 1e-9), 1),
+                   "decode_hbm_frac": round(dec_bytes / max(decode_s, 1e-9) / (HBM_PEAK_GBS * 1e9), 4),
+                   "rounds": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in s.items()} for s in last]},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(weights, shape, wl)
+    eng.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -236,6 +236,46 @@ rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t
                                 int32_t* accept_round_out, int32_t* kept_out,
                                 int32_t* n_rounds_out);
 
+/* Kernel classes of the rollout step, for rp_profile_* (bit i of a mask = class i). */
+typedef enum rp_kernel_class {
+  RP_K_EMBED_NORM = 0,   /* embedding gather + first RMSNorm */
+  RP_K_ADD_NORM = 1,     /* residual add of split-K partials + RMSNorm */
+  RP_K_GEMM_QKV = 2,
+  RP_K_ROPE_APPEND = 3,  /* q/k/v bias + RoPE + paged KV append */
+  RP_K_ATTN = 4,         /* prefill or decode attention */
+  RP_K_ATTN_MERGE = 5,   /* decode split merge */
+  RP_K_GEMM_O = 6,
+  RP_K_GEMM_GATE_UP = 7, /* with the SiLU * up epilogue */
+  RP_K_GEMM_DOWN = 8,
+  RP_K_GEMM_LM_HEAD = 9,
+  RP_K_SAMPLE = 10,
+  RP_K_COUNT = 11
+} rp_kernel_class;
+
+/* Accumulated measurements of one kernel class in one phase.  bytes and
+ * flops are the algorithmic amounts the launches had to move / compute
+ * (weights, activations, KV actually attended, outputs; split-K partials are
+ * counted once), not hardware counters. */
+typedef struct rp_kernel_stats {
+  int32_t kernel_class;  /* rp_kernel_class */
+  int32_t phase;         /* 0 prefill, 1 decode */
+  int64_t launches;
+  double total_ms;       /* sum of per-launch HIP event intervals on the engine stream */
+  double bytes;
+  double flops;
+} rp_kernel_stats;
+
+/* Per-kernel timing, the measurement side of the paper's offline profiling
+ * phase (section 4.1: prefill and decode throughput against batch size and
+ * sequence length).  class_mask selects the classes whose launches are
+ * bracketed by HIP events from now on (0 stops).  Bracketing adds a little
+ * host work per selected launch; unselected launches are untouched. */
+rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask);
+
+/* Synchronise, then report and reset the accumulated measurements: one
+ * record per (class, phase) with launches > 0, into host out [cap]. */
+rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int32_t* n_out);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* rp_last_error(void);
 

@@ -100,6 +100,8 @@ ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l) {
   p.slot_id = take(S * 8);
   p.slot_temp = take(S * 4);
   p.meta = take(static_cast<size_t>(p.meta_ints) * 4);
+  p.cand_val = take(S * static_cast<size_t>(sample_chunks(c.vocab)) * 4);
+  p.cand_idx = take(S * static_cast<size_t>(sample_chunks(c.vocab)) * 4);
   p.total = off;
   return p;
 }
@@ -240,11 +242,54 @@ void Engine::check_admission(int32_t n, const int64_t* ids, const int64_t* offs,
   if (!pool_.can_take(pages)) throw RpError(RP_ERR_OUT_OF_PAGES, "KV pool cannot hold the admitted sequences");
 }
 
+template <typename F>
+void Engine::launch_timed(int cls, double bytes, double flops, F&& launch) {
+  if (!(prof_mask_ & (1u << cls))) {
+    HIP_TRY(launch());
+    return;
+  }
+  auto take = [&]() {
+    if (prof_pool_.empty()) {
+      hipEvent_t e;
+      HIP_TRY(hipEventCreate(&e));
+      return e;
+    }
+    hipEvent_t e = prof_pool_.back();
+    prof_pool_.pop_back();
+    return e;
+  };
+  hipEvent_t e0 = take(), e1 = take();
+  HIP_TRY(hipEventRecord(e0, stream_));
+  HIP_TRY(launch());
+  HIP_TRY(hipEventRecord(e1, stream_));
+  prof_pending_.push_back({cls, phase_, e0, e1, bytes, flops});
+  if (prof_pending_.size() >= 4096) prof_harvest();
+}
+
+void Engine::prof_harvest() {
+  if (prof_pending_.empty()) return;
+  HIP_TRY(hipEventSynchronize(prof_pending_.back().e1));
+  for (auto& r : prof_pending_) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, r.e0, r.e1));
+    ProfAcc& a = prof_acc_[r.cls][r.phase];
+    a.launches += 1;
+    a.ms += ms;
+    a.bytes += r.bytes;
+    a.flops += r.flops;
+    prof_pool_.push_back(r.e0);
+    prof_pool_.push_back(r.e1);
+  }
+  prof_pending_.clear();
+}
+
 void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_splits, int tps) {
   const int H = cfg_.hidden, I = cfg_.intermediate, V = cfg_.vocab, hd = cfg_.head_dim;
   const int nq = cfg_.n_q_heads, nkv = cfg_.n_kv_heads;
   const float eps = cfg_.rms_eps;
+  const double e = static_cast<double>(esz_);
   hipStream_t s = stream_;
+  phase_ = pre ? 0 : 1;
   float* x = sp<float>(plan_.x);
   void* h = scratch_ + plan_.h;
   float* part = sp<float>(plan_.part);
@@ -260,13 +305,26 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     if (static_cast<size_t>(sp_) > cap) sp_ = static_cast<int>(std::max<size_t>(cap, 1));
     return sp_;
   };
+  // Algorithmic traffic of C[M,N] = A[M,K] W[N,K]^T: weights and activations
+  // read once, the fp32 (or storage-type) result written once.
+  auto gemm_bytes = [&](double m, double n, double k, double out_esz) { return (n * k + m * k) * e + m * n * out_esz; };
+  const double Md = M;
 
   EmbedArgs ea{w_.embed, layers_[0].attn_norm, m_in_tok_, m_slot_, tokens_cur, M, H, eps, x, h};
-  HIP_TRY(launch_embed_norm(bf16_, ea, s));
+  launch_timed(RP_K_EMBED_NORM, Md * H * (2 * e + 4), 0, [&] { return launch_embed_norm(bf16_, ea, s); });
 
   const int s_qkv = splits_for(nqkv_, H);
   const int s_o = splits_for(H, nq * hd);
   const int s_d = splits_for(H, I);
+  const double kv_tok_bytes = 2.0 * nkv * hd * e;  // one layer's K and V of one token
+  double attn_bytes, attn_flops;
+  if (pre) {
+    attn_bytes = Md * kv_tok_bytes + 2.0 * Md * nq * hd * e;
+    attn_flops = 2.0 * nq * hd * sum_ctx_sq_;
+  } else {
+    attn_bytes = sum_ctx_ * kv_tok_bytes + 2.0 * Md * nq * hd * e;
+    attn_flops = 4.0 * nq * hd * sum_ctx_;
+  }
   for (int l = 0; l < cfg_.n_layers; ++l) {
     const rp_layer_weights& L = layers_[l];
     char* kpool = kv_ + static_cast<size_t>(l) * layer_kv_bytes_;
@@ -276,11 +334,12 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     g.A = h; g.lda = H; g.M = M; g.N = nqkv_; g.K = H;
     g.W = WSeg{{L.wq, L.wk, L.wv}, {nq * hd, nkv * hd, nkv * hd}, 3};
     g.epi = kEpiPartial; g.splits = s_qkv; g.part = part;
-    HIP_TRY(launch_gemm(bf16_, g, s));
+    launch_timed(RP_K_GEMM_QKV, gemm_bytes(Md, nqkv_, H, 4), 2.0 * Md * nqkv_ * H,
+                 [&] { return launch_gemm(bf16_, g, s); });
 
     RopeArgs ra{part, s_qkv, M, L.bq, L.bk, L.bv, nq, nkv, hd, m_pos_, m_slot_, pt, plan_.max_pages,
                 sp<float>(plan_.rope_cos), sp<float>(plan_.rope_sin), q, kpool, vpool};
-    HIP_TRY(launch_rope_append(bf16_, ra, s));
+    launch_timed(RP_K_ROPE_APPEND, Md * nqkv_ * (4.0 + e), 0, [&] { return launch_rope_append(bf16_, ra, s); });
 
     AttnArgs aa{};
     aa.q = q; aa.k_pool = kpool; aa.v_pool = vpool; aa.page_table = pt; aa.pt_stride = plan_.max_pages;
@@ -290,39 +349,44 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     if (pre) {
       aa.n_seq = n_seq; aa.seq_slot = m_seq_slot_; aa.seq_row0 = m_seq_row0_; aa.seq_pos0 = m_seq_pos0_;
       aa.seq_ntok = m_seq_ntok_; aa.item_off = m_item_off_; aa.total_items = total_items;
-      HIP_TRY(launch_attn_prefill(bf16_, aa, s));
+      launch_timed(RP_K_ATTN, attn_bytes, attn_flops, [&] { return launch_attn_prefill(bf16_, aa, s); });
     } else {
       aa.B = M; aa.row_slot = m_slot_; aa.row_ctx = m_ctx_; aa.split_off = m_split_off_;
       aa.total_splits = total_splits; aa.tokens_per_split = tps;
       aa.part_o = sp<float>(plan_.att_o); aa.part_ml = sp<float>(plan_.att_ml);
-      HIP_TRY(launch_attn_decode(bf16_, aa, s));
-      if (bf16_) HIP_TRY(launch_attn_merge(aa, s));
+      launch_timed(RP_K_ATTN, attn_bytes, attn_flops, [&] { return launch_attn_decode(bf16_, aa, s); });
+      if (bf16_) {
+        const double pbytes = static_cast<double>(total_splits) * nkv * (nq / nkv) * (hd + 2.0) * 4;
+        launch_timed(RP_K_ATTN_MERGE, pbytes + Md * nq * hd * e, 0, [&] { return launch_attn_merge(aa, s); });
+      }
     }
 
     g = GemmArgs{};
     g.A = attn; g.lda = nq * hd; g.M = M; g.N = H; g.K = nq * hd;
     g.W = WSeg{{L.wo, nullptr, nullptr}, {H, 0, 0}, 1};
     g.epi = kEpiPartial; g.splits = s_o; g.part = part;
-    HIP_TRY(launch_gemm(bf16_, g, s));
+    launch_timed(RP_K_GEMM_O, gemm_bytes(Md, H, nq * hd, 4), 2.0 * Md * H * nq * hd,
+                 [&] { return launch_gemm(bf16_, g, s); });
 
     AddNormArgs an{x, part, s_o, L.mlp_norm, M, H, eps, h};
-    HIP_TRY(launch_add_rmsnorm(bf16_, an, s));
+    launch_timed(RP_K_ADD_NORM, Md * H * (4.0 * 3 + e), 0, [&] { return launch_add_rmsnorm(bf16_, an, s); });
 
     g = GemmArgs{};
     g.A = h; g.lda = H; g.M = M; g.N = I; g.K = H;
     g.W = WSeg{{L.w_gate, L.w_up, nullptr}, {I, I, 0}, 2};
     g.epi = kEpiSiluMul; g.splits = 1; g.act_out = act;
-    HIP_TRY(launch_gemm(bf16_, g, s));
+    launch_timed(RP_K_GEMM_GATE_UP, gemm_bytes(Md, 2.0 * I, H, 0) + Md * I * e, 4.0 * Md * I * H,
+                 [&] { return launch_gemm(bf16_, g, s); });
 
     g = GemmArgs{};
     g.A = act; g.lda = I; g.M = M; g.N = H; g.K = I;
     g.W = WSeg{{L.w_down, nullptr, nullptr}, {H, 0, 0}, 1};
     g.epi = kEpiPartial; g.splits = s_d; g.part = part;
-    HIP_TRY(launch_gemm(bf16_, g, s));
+    launch_timed(RP_K_GEMM_DOWN, gemm_bytes(Md, H, I, 4), 2.0 * Md * H * I, [&] { return launch_gemm(bf16_, g, s); });
 
     const void* next_norm = (l + 1 < cfg_.n_layers) ? layers_[l + 1].attn_norm : w_.final_norm;
     AddNormArgs an2{x, part, s_d, next_norm, M, H, eps, h};
-    HIP_TRY(launch_add_rmsnorm(bf16_, an2, s));
+    launch_timed(RP_K_ADD_NORM, Md * H * (4.0 * 3 + e), 0, [&] { return launch_add_rmsnorm(bf16_, an2, s); });
   }
 
   const void* lm_in = h;
@@ -336,12 +400,14 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
   g.A = lm_in; g.lda = H; g.M = m_lm; g.N = V; g.K = H;
   g.W = WSeg{{w_.lm_head, nullptr, nullptr}, {V, 0, 0}, 1};
   g.epi = kEpiPartial; g.splits = 1; g.part = sp<float>(plan_.logits);
-  HIP_TRY(launch_gemm(bf16_, g, s));
+  launch_timed(RP_K_GEMM_LM_HEAD, gemm_bytes(m_lm, V, H, 4), 2.0 * m_lm * V * H,
+               [&] { return launch_gemm(bf16_, g, s); });
 
   SampleArgs sa{sp<float>(plan_.logits), m_lm, V, m_gen_slot_, m_gen_pos_, m_gen_hist_,
                 sp<uint64_t>(plan_.slot_seed), sp<uint64_t>(plan_.slot_id), sp<float>(plan_.slot_temp),
-                tokens_cur, sp<int32_t>(plan_.hist), lim_.max_context};
-  HIP_TRY(launch_sample(sa, s));
+                tokens_cur, sp<int32_t>(plan_.hist), lim_.max_context, sp<float>(plan_.cand_val),
+                sp<int32_t>(plan_.cand_idx)};
+  launch_timed(RP_K_SAMPLE, static_cast<double>(m_lm) * V * 4, 0, [&] { return launch_sample(sa, s); });
 }
 
 void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t* toks, const int64_t* offs,
@@ -364,6 +430,7 @@ void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t*
   int32_t* gen_hist = gen_pos + n;
   const int tpi = attn_prefill_tokens_per_item(bf16_, cfg_.n_q_heads / cfg_.n_kv_heads);
   int row = 0, items = 0;
+  sum_ctx_sq_ = 0;
   for (int j = 0; j < n; ++j) {
     const int64_t o = offs[seq_index[j]];
     const int p = static_cast<int>(offs[seq_index[j] + 1] - o);
@@ -376,6 +443,7 @@ void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t*
     seq_row0[j] = row;
     seq_pos0[j] = 0;
     seq_ntok[j] = p;
+    sum_ctx_sq_ += static_cast<double>(p) * (p + 1);
     item_off[j] = items;
     items += (p + tpi - 1) / tpi;
     last_row[j] = row + p - 1;
@@ -476,6 +544,7 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
   int32_t* gen_pos = split_off + B + 1;
   int32_t* gen_hist = gen_pos + B;
   int64_t total_pages = 0;
+  sum_ctx_ = 0;
   for (int i = 0; i < B; ++i) {
     const Seq& q = slots_[rows[i]];
     in_tok[i] = forced ? forced[i] : -1;
@@ -485,6 +554,7 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     gen_pos[i] = pos[i] + 1;
     gen_hist[i] = q.n_gen;
     total_pages += PagePool::pages_for(ctx[i], kPageTokens);
+    sum_ctx_ += ctx[i];
   }
   int tps = 0, total_splits = 0;
   if (bf16_) {
@@ -516,6 +586,27 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     if (q.n_gen >= q.max_new) q.finished = true;
   }
   return B;
+}
+
+void Engine::profile_enable(uint32_t mask) {
+  if (mask >> RP_K_COUNT) throw RpError(RP_ERR_INVALID_ARG, "profile mask names an unknown kernel class");
+  prof_mask_ = mask;
+}
+
+int32_t Engine::profile_read(rp_kernel_stats* out, int32_t cap) {
+  if (cap < 0 || (cap > 0 && !out)) throw RpError(RP_ERR_INVALID_ARG, "profile_read: bad output");
+  HIP_TRY(hipStreamSynchronize(stream_));
+  prof_harvest();
+  int32_t n = 0;
+  for (int c = 0; c < RP_K_COUNT; ++c)
+    for (int ph = 0; ph < 2; ++ph) {
+      ProfAcc& a = prof_acc_[c][ph];
+      if (a.launches == 0) continue;
+      if (n < cap) out[n] = rp_kernel_stats{c, ph, a.launches, a.ms, a.bytes, a.flops};
+      ++n;
+      a = ProfAcc{};
+    }
+  return std::min(n, cap);
 }
 
 void Engine::release(int32_t slot) {

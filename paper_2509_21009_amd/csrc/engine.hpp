@@ -23,7 +23,7 @@ struct RpError : std::runtime_error {
 // Byte offsets of every buffer carved from the caller's scratch workspace.
 struct ScratchPlan {
   size_t x, h, part, q, attn, act, hsel, logits, att_o, att_ml, rope_cos, rope_sin, page_table,
-      tokens_cur, hist, resp, slot_seed, slot_id, slot_temp, meta;
+      tokens_cur, hist, resp, slot_seed, slot_id, slot_temp, meta, cand_val, cand_idx;
   size_t total;
   size_t part_elems;
   int32_t split_cap;   // decode attention work-item capacity (splits)
@@ -67,6 +67,9 @@ class Engine {
   int32_t rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
                   const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
                   int32_t* resp_out, rp_round_stats* stats, int32_t max_stats);
+
+  void profile_enable(uint32_t mask);
+  int32_t profile_read(rp_kernel_stats* out, int32_t cap);
 
   bool broken() const { return broken_; }
   void mark_broken() { broken_ = true; }
@@ -127,6 +130,26 @@ class Engine {
                 *m_item_off_ = nullptr, *m_last_row_ = nullptr, *m_gen_pos_ = nullptr,
                 *m_gen_hist_ = nullptr, *m_gen_slot_ = nullptr;
   std::vector<hipEvent_t> events_;
+
+  // per-kernel-class profiling (rp_profile_*)
+  struct ProfRec {
+    int cls, phase;
+    hipEvent_t e0, e1;
+    double bytes, flops;
+  };
+  struct ProfAcc {
+    int64_t launches = 0;
+    double ms = 0, bytes = 0, flops = 0;
+  };
+  template <typename F> void launch_timed(int cls, double bytes, double flops, F&& launch);
+  void prof_harvest();
+  uint32_t prof_mask_ = 0;
+  int phase_ = 0;             // 0 prefill, 1 decode
+  double sum_ctx_ = 0;        // attended KV tokens of the current forward (decode)
+  double sum_ctx_sq_ = 0;     // sum of squared prompt lengths (prefill attention)
+  std::vector<ProfRec> prof_pending_;
+  std::vector<hipEvent_t> prof_pool_;
+  ProfAcc prof_acc_[RP_K_COUNT][2];
 };
 
 }  // namespace rollpack

@@ -155,25 +155,46 @@ __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
   }
 }
 
+// One block per (row, query head): the splits' maxima and sums are staged in
+// LDS, then every output element accumulates its weighted partials with the
+// loads of several splits in flight.
+constexpr int kMergeCache = 512;
+
 template <int HD>
 __global__ __launch_bounds__(128) void k_attn_merge(AttnArgs a) {
+  __shared__ float sm[kMergeCache], sl[kMergeCache];
+  __shared__ float red[2];
   const int b = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
   const int G = a.n_q / a.n_kv;
   const int kh = h / G, c = h % G;
-  const int s0 = a.split_off[b], s1 = a.split_off[b + 1];
-  float mx = -INFINITY;
-  for (int s = s0; s < s1; ++s) mx = fmaxf(mx, a.part_ml[(static_cast<size_t>(s) * a.n_kv + kh) * 32 + c]);
-  float num = 0.f, den = 0.f;
-  for (int s = s0; s < s1; ++s) {
-    const size_t item = static_cast<size_t>(s) * a.n_kv + kh;
-    const float ms = a.part_ml[item * 32 + c];
-    if (ms == -INFINITY) continue;
-    const float w = exp2f(ms - mx);
-    den += w * a.part_ml[item * 32 + 16 + c];
-    if (d < HD) num += w * a.part_o[(item * 16 + c) * HD + d];
+  const int s0 = a.split_off[b], n = a.split_off[b + 1] - s0;
+  const int nc = min(n, kMergeCache);
+  for (int t = threadIdx.x; t < nc; t += blockDim.x) {
+    const size_t item = static_cast<size_t>(s0 + t) * a.n_kv + kh;
+    sm[t] = a.part_ml[item * 32 + c];
+    sl[t] = a.part_ml[item * 32 + 16 + c];
   }
-  if (d < HD)
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int t = threadIdx.x; t < n; t += blockDim.x)
+    mx = fmaxf(mx, t < nc ? sm[t] : a.part_ml[(static_cast<size_t>(s0 + t) * a.n_kv + kh) * 32 + c]);
+  mx = wave_max(mx);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(red[0], red[1]);
+  float num = 0.f, den = 0.f;
+  if (d < HD) {
+#pragma unroll 8
+    for (int t = 0; t < n; ++t) {
+      const size_t item = static_cast<size_t>(s0 + t) * a.n_kv + kh;
+      const float ms = t < nc ? sm[t] : a.part_ml[item * 32 + c];
+      const float ls = t < nc ? sl[t] : a.part_ml[item * 32 + 16 + c];
+      const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
+      den += w * ls;
+      num += w * a.part_o[(item * 16 + c) * HD + d];
+    }
     static_cast<bf16_t*>(a.out)[(static_cast<size_t>(b) * a.n_q + h) * HD + d] = f32_to_bf16(num / den);
+  }
 }
 
 template <int HD>

@@ -1,7 +1,8 @@
 // Row-wise kernels of the decoder step: embedding + RMSNorm, residual add +
 // RMSNorm, q/k/v bias + RoPE + paged KV append, and Gumbel-max sampling with
-// a Philox4x64-10 counter-based generator.  All are bandwidth-light: one
-// 256-thread block per token row.
+// a Philox4x64-10 counter-based generator.  They move little data, so they
+// are written for latency: every load of a thread is issued before the first
+// use, and small batches are spread over several blocks per row.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -9,100 +10,176 @@ namespace rollpack {
 
 namespace {
 
+// Rows are processed by one block of up to 1024 threads, each owning two
+// 4-element chunks, so every load of a row is in flight at once.
+constexpr int kRowChunks = 2;
+
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  static __device__ __forceinline__ float4 load(const float* p, size_t i) { return *reinterpret_cast<const float4*>(p + i); }
+  static __device__ __forceinline__ void store(float* p, size_t i, float4 v) { *reinterpret_cast<float4*>(p + i) = v; }
+};
+template <> struct Vec4<bf16_t> {
+  static __device__ __forceinline__ float4 load(const bf16_t* p, size_t i) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p + i);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+  }
+  static __device__ __forceinline__ void store(bf16_t* p, size_t i, float4 v) {
+    uint2 u;
+    u.x = static_cast<uint32_t>(f32_to_bf16(v.x)) | (static_cast<uint32_t>(f32_to_bf16(v.y)) << 16);
+    u.y = static_cast<uint32_t>(f32_to_bf16(v.z)) | (static_cast<uint32_t>(f32_to_bf16(v.w)) << 16);
+    *reinterpret_cast<uint2*>(p + i) = u;
+  }
+};
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+// x holds the row (kRowChunks float4 per thread); writes h = x * rsqrt(mean(x^2)+eps) * g.
 template <typename T>
-__global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
-  __shared__ float red[4];
+__device__ __forceinline__ void norm_store(const float4 (&xv)[kRowChunks], int H, float eps, const T* g, T* h,
+                                           float* red) {
+  const int nc = H / 4;
+  float ss = 0.f;
+#pragma unroll
+  for (int v = 0; v < kRowChunks; ++v) {
+    const int c = threadIdx.x + v * blockDim.x;
+    if (c < nc) ss += xv[v].x * xv[v].x + xv[v].y * xv[v].y + xv[v].z * xv[v].z + xv[v].w * xv[v].w;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / H + eps);
+#pragma unroll
+  for (int v = 0; v < kRowChunks; ++v) {
+    const int c = threadIdx.x + v * blockDim.x;
+    if (c < nc) {
+      const float4 gv = Vec4<T>::load(g, 4 * c);
+      Vec4<T>::store(h, 4 * static_cast<size_t>(c),
+                     make_float4(xv[v].x * inv * gv.x, xv[v].y * inv * gv.y, xv[v].z * inv * gv.z, xv[v].w * inv * gv.w));
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(1024) void k_embed_norm(EmbedArgs a) {
+  __shared__ float red[16];
   const int i = blockIdx.x;
   int tok = a.in_tok[i];
   if (tok < 0) tok = a.tokens_cur[a.row_slot[i]];
   const T* e = static_cast<const T*>(a.embed) + static_cast<size_t>(tok) * a.H;
   float* x = a.x + static_cast<size_t>(i) * a.H;
-  float ss = 0.f;
-  for (int d = threadIdx.x; d < a.H; d += 256) {
-    const float v = Elem<T>::load(e, d);
-    x[d] = v;
-    ss += v * v;
+  const int nc = a.H / 4;
+  float4 xv[kRowChunks];
+#pragma unroll
+  for (int v = 0; v < kRowChunks; ++v) {
+    const int c = threadIdx.x + v * blockDim.x;
+    if (c < nc) {
+      xv[v] = Vec4<T>::load(e, 4 * c);
+      *reinterpret_cast<float4*>(x + 4 * c) = xv[v];
+    }
   }
-  ss = block256_sum(ss, red);
-  const float inv = 1.0f / sqrtf(ss / a.H + a.eps);
-  const T* g = static_cast<const T*>(a.norm_g);
-  T* h = static_cast<T*>(a.h) + static_cast<size_t>(i) * a.H;
-  for (int d = threadIdx.x; d < a.H; d += 256) Elem<T>::store(h, d, x[d] * inv * Elem<T>::load(g, d));
+  norm_store<T>(xv, a.H, a.eps, static_cast<const T*>(a.norm_g), static_cast<T*>(a.h) + static_cast<size_t>(i) * a.H,
+                red);
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_add_rmsnorm(AddNormArgs a) {
-  __shared__ float red[4];
+template <typename T, int S>
+__global__ __launch_bounds__(1024) void k_add_rmsnorm(AddNormArgs a) {
+  __shared__ float red[16];
   const int i = blockIdx.x;
   float* x = a.x + static_cast<size_t>(i) * a.H;
+  const int nc = a.H / 4;
   const size_t plane = static_cast<size_t>(a.M) * a.H;
-  float ss = 0.f;
-  for (int d = threadIdx.x; d < a.H; d += 256) {
-    float v = x[d];
-    if (a.part) {
-      const float* p = a.part + static_cast<size_t>(i) * a.H + d;
-      for (int s = 0; s < a.splits; ++s) v += p[s * plane];
-      x[d] = v;
+  float4 xv[kRowChunks];
+  float4 pv[S > 0 ? S : 1][kRowChunks];
+#pragma unroll
+  for (int v = 0; v < kRowChunks; ++v) {
+    const int c = threadIdx.x + v * blockDim.x;
+    if (c < nc) {
+      xv[v] = *reinterpret_cast<const float4*>(x + 4 * c);
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        pv[s][v] = *reinterpret_cast<const float4*>(a.part + s * plane + static_cast<size_t>(i) * a.H + 4 * c);
     }
-    ss += v * v;
   }
-  ss = block256_sum(ss, red);
-  const float inv = 1.0f / sqrtf(ss / a.H + a.eps);
-  const T* g = static_cast<const T*>(a.norm_g);
-  T* h = static_cast<T*>(a.h) + static_cast<size_t>(i) * a.H;
-  for (int d = threadIdx.x; d < a.H; d += 256) Elem<T>::store(h, d, x[d] * inv * Elem<T>::load(g, d));
+  if (S > 0) {
+#pragma unroll
+    for (int v = 0; v < kRowChunks; ++v) {
+      const int c = threadIdx.x + v * blockDim.x;
+      if (c < nc) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          xv[v].x += pv[s][v].x; xv[v].y += pv[s][v].y; xv[v].z += pv[s][v].z; xv[v].w += pv[s][v].w;
+        }
+        *reinterpret_cast<float4*>(x + 4 * c) = xv[v];
+      }
+    }
+  }
+  norm_store<T>(xv, a.H, a.eps, static_cast<const T*>(a.norm_g), static_cast<T*>(a.h) + static_cast<size_t>(i) * a.H,
+                red);
 }
 
-template <typename T>
+// One thread per rotated (q or k) pair or per v element; blockIdx.y strides
+// the row's items so small batches still fill the GPU.
+template <typename T, int S>
 __global__ __launch_bounds__(256) void k_rope_append(RopeArgs a) {
   const int i = blockIdx.x;
   const int hd = a.hd, half = hd / 2;
   const int nq_el = a.n_q * hd, nk_el = a.n_kv * hd;
   const int nqkv = nq_el + 2 * nk_el;
+  const int n_pairs = (a.n_q + a.n_kv) * half;
+  const int t = blockIdx.y * blockDim.x + threadIdx.x;
+  if (t >= n_pairs + nk_el) return;
   const size_t plane = static_cast<size_t>(a.M) * nqkv;
-  const float* prow = a.part + static_cast<size_t>(i) * nqkv;
+  const float* __restrict__ prow = a.part + static_cast<size_t>(i) * nqkv;
   const int pos = a.pos[i];
   const int slot = a.slot[i];
   const int page = a.page_table[static_cast<size_t>(slot) * a.pt_stride + pos / kPageTokens];
   const int off = pos % kPageTokens;
-  const T* bq = static_cast<const T*>(a.bq);
-  const T* bk = static_cast<const T*>(a.bk);
-  const T* bv = static_cast<const T*>(a.bv);
-  auto value = [&](int n) {
-    float v = 0.f;
-    for (int s = 0; s < a.splits; ++s) v += prow[s * plane + n];
-    if (n < nq_el) return v + Elem<T>::load(bq, n);
-    if (n < nq_el + nk_el) return v + Elem<T>::load(bk, n - nq_el);
-    return v + Elem<T>::load(bv, n - nq_el - nk_el);
-  };
-  const float* cs = a.rope_cos + static_cast<size_t>(pos) * half;
-  const float* sn = a.rope_sin + static_cast<size_t>(pos) * half;
-  T* q = static_cast<T*>(a.q_out) + static_cast<size_t>(i) * nq_el;
-  T* kp = static_cast<T*>(a.k_pool);
-  T* vp = static_cast<T*>(a.v_pool);
-  // Rotate-half RoPE on q and k heads (k heads follow q heads in the qkv row).
-  for (int t = threadIdx.x; t < (a.n_q + a.n_kv) * half; t += 256) {
+  if (t < n_pairs) {
     const int head = t / half, d = t % half;
-    const int n1 = head * hd + d;
-    const float u1 = value(n1), u2 = value(n1 + half);
-    const float c = cs[d], s = sn[d];
-    const float r1 = u1 * c - u2 * s;
-    const float r2 = u2 * c + u1 * s;
+    const int n1 = head * hd + d, n2 = n1 + half;
+    float u1 = 0.f, u2 = 0.f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      u1 += prow[s * plane + n1];
+      u2 += prow[s * plane + n2];
+    }
+    const bool isq = head < a.n_q;
+    const T* b = isq ? static_cast<const T*>(a.bq) : static_cast<const T*>(a.bk);
+    const int bi = isq ? n1 : n1 - nq_el;
+    u1 += Elem<T>::load(b, bi);
+    u2 += Elem<T>::load(b, bi + half);
+    const float c = a.rope_cos[static_cast<size_t>(pos) * half + d];
+    const float sn = a.rope_sin[static_cast<size_t>(pos) * half + d];
+    const float r1 = u1 * c - u2 * sn;
+    const float r2 = u2 * c + u1 * sn;
     if (head < a.n_q) {
+      T* q = static_cast<T*>(a.q_out) + static_cast<size_t>(i) * nq_el;
       Elem<T>::store(q, n1, r1);
-      Elem<T>::store(q, n1 + half, r2);
+      Elem<T>::store(q, n2, r2);
     } else {
       const int kh = head - a.n_q;
       const size_t base = ((static_cast<size_t>(page) * a.n_kv + kh) * kPageTokens + off) * hd;
-      Elem<T>::store(kp, base + d, r1);
-      Elem<T>::store(kp, base + d + half, r2);
+      Elem<T>::store(static_cast<T*>(a.k_pool), base + d, r1);
+      Elem<T>::store(static_cast<T*>(a.k_pool), base + d + half, r2);
     }
-  }
-  for (int t = threadIdx.x; t < nk_el; t += 256) {
-    const int kh = t / hd, d = t % hd;
-    const float v = value(nq_el + nk_el + t);
+  } else {
+    const int e = t - n_pairs;
+    const int kh = e / hd, d = e % hd;
+    const int n = nq_el + nk_el + e;
+    float v = 0.f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) v += prow[s * plane + n];
+    v += Elem<T>::load(static_cast<const T*>(a.bv), e);
     const size_t idx = ((static_cast<size_t>(page) * a.n_kv + kh) * hd + d) * kPageTokens + off;
-    Elem<T>::store(vp, idx, v);
+    Elem<T>::store(static_cast<T*>(a.v_pool), idx, v);
   }
 }
 
@@ -137,7 +214,12 @@ __device__ __forceinline__ void take_best(float& bv, int& bi, float v, int i) {
   if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
 }
 
-__global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
+// Pass 1: block (row, chunk) scores kSampleChunk vocabulary entries and
+// writes its best (score, index).  Pass 2: one wave per row reduces the
+// chunk winners (ties -> lowest index) and records the token.
+constexpr int kSampleChunk = 2048;
+
+__global__ __launch_bounds__(256) void k_sample_partial(SampleArgs a) {
   __shared__ float sv[4];
   __shared__ int si[4];
   const int row = blockIdx.x;
@@ -146,24 +228,29 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   const float* l = a.logits + static_cast<size_t>(row) * a.V;
   float best = -INFINITY;
   int besti = 0x7fffffff;
+  const int v0 = blockIdx.y * kSampleChunk;
   if (temp == 0.f) {
-    for (int v = threadIdx.x; v < a.V; v += 256) take_best(best, besti, l[v], v);
+#pragma unroll
+    for (int e = 0; e < kSampleChunk / 256; ++e) {
+      const int v = v0 + e * 256 + threadIdx.x;
+      if (v < a.V) take_best(best, besti, l[v], v);
+    }
   } else {
     const float inv_t = 1.0f / temp;
-    const uint64_t key0 = a.slot_seed[slot], key1 = a.slot_id[slot];
-    const uint64_t pos = static_cast<uint64_t>(a.row_pos[row]);
-    const int groups = (a.V + 7) / 8;
-    for (int gi = threadIdx.x; gi < groups; gi += 256) {
-      uint64_t x0 = pos, x1 = static_cast<uint64_t>(gi), x2 = 0, x3 = 0;
-      philox4x64_10(x0, x1, x2, x3, key0, key1);
+    const int gi = (v0 >> 3) + threadIdx.x;   // 8 entries per thread, one Philox block
+    const int vb = gi * 8;
+    if (vb < a.V) {
+      float lv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) lv[e] = (vb + e < a.V) ? l[vb + e] : -INFINITY;
+      uint64_t x0 = static_cast<uint64_t>(a.row_pos[row]), x1 = static_cast<uint64_t>(gi), x2 = 0, x3 = 0;
+      philox4x64_10(x0, x1, x2, x3, a.slot_seed[slot], a.slot_id[slot]);
       const uint64_t outs[4] = {x0, x1, x2, x3};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int v = gi * 8 + e;
-        if (v < a.V) {
-          const uint32_t w = (e & 1) ? static_cast<uint32_t>(outs[e >> 1] >> 32)
-                                     : static_cast<uint32_t>(outs[e >> 1]);
-          take_best(best, besti, l[v] * inv_t + word_to_gumbel(w), v);
+        if (vb + e < a.V) {
+          const uint32_t w = (e & 1) ? static_cast<uint32_t>(outs[e >> 1] >> 32) : static_cast<uint32_t>(outs[e >> 1]);
+          take_best(best, besti, lv[e] * inv_t + word_to_gumbel(w), vb + e);
         }
       }
     }
@@ -178,7 +265,26 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int w = 1; w < 4; ++w) take_best(best, besti, sv[w], si[w]);
+    a.cand_val[static_cast<size_t>(row) * gridDim.y + blockIdx.y] = best;
+    a.cand_idx[static_cast<size_t>(row) * gridDim.y + blockIdx.y] = besti;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_sample_final(SampleArgs a, int chunks) {
+  const int row = blockIdx.x;
+  float best = -INFINITY;
+  int besti = 0x7fffffff;
+  for (int c = threadIdx.x; c < chunks; c += 64)
+    take_best(best, besti, a.cand_val[static_cast<size_t>(row) * chunks + c], a.cand_idx[static_cast<size_t>(row) * chunks + c]);
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(best, m, 64);
+    const int oi = __shfl_xor(besti, m, 64);
+    take_best(best, besti, ov, oi);
+  }
+  if (threadIdx.x == 0) {
     if (besti == 0x7fffffff) besti = 0;  // all-NaN row: deterministic fallback
+    const int slot = a.row_slot[row];
     a.tokens_cur[slot] = besti;
     a.hist[static_cast<size_t>(slot) * a.hist_stride + a.row_hist[row]] = besti;
   }
@@ -199,30 +305,83 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint8_t* src, const i
 
 }  // namespace
 
+namespace {
+int row_threads(int H) {
+  int t = (H / 4 + kRowChunks - 1) / kRowChunks;
+  t = (t + 63) / 64 * 64;
+  return t < 64 ? 64 : t;
+}
+
+template <typename T, int S>
+void launch_add_norm_s(const AddNormArgs& a, int threads, hipStream_t s) {
+  hipLaunchKernelGGL((k_add_rmsnorm<T, S>), dim3(a.M), dim3(threads), 0, s, a);
+}
+
+template <typename T>
+hipError_t launch_add_norm_t(const AddNormArgs& a, hipStream_t s) {
+  const int th = row_threads(a.H);
+  const int S = a.part ? a.splits : 0;
+  switch (S) {
+    case 0: launch_add_norm_s<T, 0>(a, th, s); break;
+    case 1: launch_add_norm_s<T, 1>(a, th, s); break;
+    case 2: launch_add_norm_s<T, 2>(a, th, s); break;
+    case 3: launch_add_norm_s<T, 3>(a, th, s); break;
+    case 4: launch_add_norm_s<T, 4>(a, th, s); break;
+    case 5: launch_add_norm_s<T, 5>(a, th, s); break;
+    case 6: launch_add_norm_s<T, 6>(a, th, s); break;
+    case 7: launch_add_norm_s<T, 7>(a, th, s); break;
+    case 8: launch_add_norm_s<T, 8>(a, th, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_rope_t(const RopeArgs& a, hipStream_t s) {
+  const int items = (a.n_q + a.n_kv) * (a.hd / 2) + a.n_kv * a.hd;
+  dim3 grid(a.M, (items + 255) / 256);
+  switch (a.splits) {
+    case 1: hipLaunchKernelGGL((k_rope_append<T, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_rope_append<T, 2>), grid, dim3(256), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_rope_append<T, 3>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_rope_append<T, 4>), grid, dim3(256), 0, s, a); break;
+    case 5: hipLaunchKernelGGL((k_rope_append<T, 5>), grid, dim3(256), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_rope_append<T, 6>), grid, dim3(256), 0, s, a); break;
+    case 7: hipLaunchKernelGGL((k_rope_append<T, 7>), grid, dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_rope_append<T, 8>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_embed_norm(int bf16, const EmbedArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (bf16) hipLaunchKernelGGL(k_embed_norm<bf16_t>, dim3(a.M), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_embed_norm<float>, dim3(a.M), dim3(256), 0, s, a);
+  if (a.H % 4 || a.H > 4 * kRowChunks * 1024) return hipErrorInvalidValue;
+  const int th = row_threads(a.H);
+  if (bf16) hipLaunchKernelGGL(k_embed_norm<bf16_t>, dim3(a.M), dim3(th), 0, s, a);
+  else hipLaunchKernelGGL(k_embed_norm<float>, dim3(a.M), dim3(th), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_add_rmsnorm(int bf16, const AddNormArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (bf16) hipLaunchKernelGGL(k_add_rmsnorm<bf16_t>, dim3(a.M), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_add_rmsnorm<float>, dim3(a.M), dim3(256), 0, s, a);
-  return hipGetLastError();
+  if (a.H % 4 || a.H > 4 * kRowChunks * 1024) return hipErrorInvalidValue;
+  return bf16 ? launch_add_norm_t<bf16_t>(a, s) : launch_add_norm_t<float>(a, s);
 }
 
 hipError_t launch_rope_append(int bf16, const RopeArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (bf16) hipLaunchKernelGGL(k_rope_append<bf16_t>, dim3(a.M), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_rope_append<float>, dim3(a.M), dim3(256), 0, s, a);
-  return hipGetLastError();
+  return bf16 ? launch_rope_t<bf16_t>(a, s) : launch_rope_t<float>(a, s);
 }
+
+int sample_chunks(int V) { return (V + kSampleChunk - 1) / kSampleChunk; }
 
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_sample, dim3(a.B), dim3(256), 0, s, a);
+  const int chunks = sample_chunks(a.V);
+  hipLaunchKernelGGL(k_sample_partial, dim3(a.B, chunks), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_sample_final, dim3(a.B), dim3(64), 0, s, a, chunks);
   return hipGetLastError();
 }
 

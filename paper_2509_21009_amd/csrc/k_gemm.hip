@@ -68,26 +68,39 @@ __global__ __launch_bounds__(256) void k_gemm_stream(GemmArgs a, int chunks_per_
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int n_chunks = K / 128;
-  const int c0 = blockIdx.y * chunks_per_split;
-  const int c1 = min(c0 + chunks_per_split, n_chunks);
-  for (int c = c0 + wave; c < c1; c += 4) {
-    const int k = c * 128 + g * 32;
-    bf16x8_t wv[R][4], av[MT][4];
+  // Register double buffering: the loads of the wave's next chunk are in
+  // flight while the MFMAs of the current one run.
+  bf16x8_t wv[2][R][4], av[2][MT][4];
+  auto load = [&](int buf, int chunk) {
+    const int k = chunk * 128 + g * 32;
 #pragma unroll
     for (int t = 0; t < R; ++t)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) wv[t][j] = load_bf16x8(wrow[t] + k + 8 * j);
+      for (int j = 0; j < 4; ++j) wv[buf][t][j] = load_bf16x8(wrow[t] + k + 8 * j);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) av[mt][j] = load_bf16x8(arow[mt] + k + 8 * j);
+      for (int j = 0; j < 4; ++j) av[buf][mt][j] = load_bf16x8(arow[mt] + k + 8 * j);
+  };
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int t = 0; t < R; ++t)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[t][mt] = mfma16x16x32(wv[t][j], av[mt][j], acc[t][mt]);
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] = mfma16x16x32(wv[buf][t][j], av[buf][mt][j], acc[t][mt]);
+  };
+  const int n_chunks = K / 128;
+  const int c0 = blockIdx.y * chunks_per_split;
+  const int c1 = min(c0 + chunks_per_split, n_chunks);
+  int c = c0 + wave;
+  if (c < c1) load(0, c);
+  for (; c < c1; c += 8) {
+    if (c + 4 < c1) load(1, c + 4);
+    compute(0);
+    if (c + 4 >= c1) break;
+    if (c + 8 < c1) load(0, c + 8);
+    compute(1);
   }
 
   constexpr int NSL = R * MT * 4;

@@ -104,8 +104,10 @@ struct SampleArgs {
   const int32_t* row_hist;        // [B] index into the slot's token history
   const uint64_t* slot_seed; const uint64_t* slot_id; const float* slot_temp;
   int32_t* tokens_cur; int32_t* hist; int64_t hist_stride;
+  float* cand_val; int32_t* cand_idx;   // [B, sample_chunks(V)] per-chunk winners
 };
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
+int sample_chunks(int V);
 
 // out[i, :] = src[rows[i], :] for i < n (element size esize bytes, H elements)
 hipError_t launch_gather_rows(const void* src, const int32_t* rows, int n, int H, int esize,

@@ -181,6 +181,17 @@ rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t
   });
 }
 
+rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->profile_enable(class_mask); });
+}
+
+rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int32_t* n_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    const int32_t n = e->profile_read(out, cap);
+    if (n_out) *n_out = n;
+  });
+}
+
 const char* rp_last_error(void) { return g_last_error.c_str(); }
 
 }  // extern "C"

@@ -56,6 +56,19 @@ class RpRoundStats(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
 
 
+KERNEL_CLASSES = ("embed_norm", "add_norm", "gemm_qkv", "rope_append", "attn", "attn_merge", "gemm_o",
+                  "gemm_gate_up", "gemm_down", "gemm_lm_head", "sample")
+
+
+class RpKernelStats(ctypes.Structure):
+    _fields_ = [("kernel_class", ctypes.c_int32), ("phase", ctypes.c_int32), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double), ("bytes", ctypes.c_double), ("flops", ctypes.c_double)]
+
+    def as_dict(self) -> dict:
+        return {"kernel": KERNEL_CLASSES[self.kernel_class], "phase": ("prefill", "decode")[self.phase],
+                "launches": self.launches, "total_ms": self.total_ms, "bytes": self.bytes, "flops": self.flops}
+
+
 class RollpackError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{STATUS.get(status, status)}: {msg}")
@@ -88,6 +101,8 @@ SIGNATURES = {
     "rp_plan_tail_batching": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_int32, ctypes.c_int32,
                                              ctypes.c_float, ctypes.c_int32, ctypes.c_int32, _I32P, _I32P, _I32P,
                                              _I32P, _I32P, _I32P, _I32P, _I32P]),
+    "rp_profile_enable": (ctypes.c_int, [_P, ctypes.c_uint32]),
+    "rp_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(RpKernelStats), ctypes.c_int32, _I32P]),
     "rp_last_error": (ctypes.c_char_p, []),
 }
 
@@ -236,6 +251,21 @@ def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float):
     return rounds, acc[:n].copy(), kept[:n * r_spec].reshape(n, r_spec).astype(bool)
 
 
+def rp_profile_enable(eng: int, classes) -> None:
+    """classes: iterable of names from KERNEL_CLASSES (empty stops profiling)."""
+    mask = 0
+    for c in classes:
+        mask |= 1 << KERNEL_CLASSES.index(c)
+    _check(load_library().rp_profile_enable(eng, mask))
+
+
+def rp_profile_read(eng: int, cap: int = 64):
+    out = (RpKernelStats * cap)()
+    n = ctypes.c_int32()
+    _check(load_library().rp_profile_read(eng, out, cap, ctypes.byref(n)))
+    return [out[i].as_dict() for i in range(n.value)]
+
+
 def rp_last_error() -> str:
     return load_library().rp_last_error().decode()
 
@@ -320,6 +350,12 @@ class Engine:
 
     def get_tokens(self, seq_id: int, cap: int):
         return rp_get_tokens(self.handle, seq_id, cap)
+
+    def profile(self, classes):
+        rp_profile_enable(self.handle, classes)
+
+    def profile_read(self):
+        return rp_profile_read(self.handle)
 
     def rollout(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature, round_ids=None):
         return rp_rollout_generate(self.handle, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
