@@ -19,7 +19,7 @@ namespace rollpack {
 
 namespace {
 
-constexpr int kMaxGemmSplits = 8;
+constexpr int kMaxGemmSplits = 16;
 
 void hip_check(hipError_t e, const char* what) {
   if (e != hipSuccess) throw RpError(RP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -300,10 +300,9 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
   const int32_t* pt = sp<int32_t>(plan_.page_table);
 
   auto splits_for = [&](int N, int K) {
-    int sp_ = gemm_pick_splits(bf16_, M, N, K, kMaxGemmSplits);
     const size_t cap = plan_.part_elems / (static_cast<size_t>(M) * N);
-    if (static_cast<size_t>(sp_) > cap) sp_ = static_cast<int>(std::max<size_t>(cap, 1));
-    return sp_;
+    const int lim = static_cast<int>(std::min<size_t>(std::max<size_t>(cap, 1), kMaxGemmSplits));
+    return gemm_pick_splits(bf16_, M, N, K, false, lim);
   };
   // Algorithmic traffic of C[M,N] = A[M,K] W[N,K]^T: weights and activations
   // read once, the fp32 (or storage-type) result written once.

@@ -155,45 +155,55 @@ __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
   }
 }
 
-// One block per (row, query head): the splits' maxima and sums are staged in
-// LDS, then every output element accumulates its weighted partials with the
-// loads of several splits in flight.
+// One block per (row, query head) with HD x 8 threads: the splits' maxima
+// and sums are staged in LDS, each of 8 thread groups accumulates every 8th
+// split for all HD output elements, and the groups are summed in LDS.  Long
+// contexts at small batch have hundreds of splits, which a single serial
+// loop per element would walk one memory latency at a time.
 constexpr int kMergeCache = 512;
+constexpr int kMergeGroups = 8;
 
 template <int HD>
-__global__ __launch_bounds__(128) void k_attn_merge(AttnArgs a) {
+__global__ __launch_bounds__(HD * kMergeGroups) void k_attn_merge(AttnArgs a) {
   __shared__ float sm[kMergeCache], sl[kMergeCache];
-  __shared__ float red[2];
-  const int b = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+  __shared__ float part_num[kMergeGroups][HD];
+  __shared__ float part_den[kMergeGroups];
+  __shared__ float wmax[HD * kMergeGroups / 64];
+  const int b = blockIdx.x, h = blockIdx.y;
+  const int d = threadIdx.x % HD, q = threadIdx.x / HD;
   const int G = a.n_q / a.n_kv;
   const int kh = h / G, c = h % G;
   const int s0 = a.split_off[b], n = a.split_off[b + 1] - s0;
   const int nc = min(n, kMergeCache);
-  for (int t = threadIdx.x; t < nc; t += blockDim.x) {
-    const size_t item = static_cast<size_t>(s0 + t) * a.n_kv + kh;
-    sm[t] = a.part_ml[item * 32 + c];
-    sl[t] = a.part_ml[item * 32 + 16 + c];
-  }
-  __syncthreads();
+  auto m_of = [&](int t) { return a.part_ml[(static_cast<size_t>(s0 + t) * a.n_kv + kh) * 32 + c]; };
+  auto l_of = [&](int t) { return a.part_ml[(static_cast<size_t>(s0 + t) * a.n_kv + kh) * 32 + 16 + c]; };
   float mx = -INFINITY;
-  for (int t = threadIdx.x; t < n; t += blockDim.x)
-    mx = fmaxf(mx, t < nc ? sm[t] : a.part_ml[(static_cast<size_t>(s0 + t) * a.n_kv + kh) * 32 + c]);
+  for (int t = threadIdx.x; t < n; t += blockDim.x) {
+    const float mv = m_of(t);
+    if (t < nc) { sm[t] = mv; sl[t] = l_of(t); }
+    mx = fmaxf(mx, mv);
+  }
   mx = wave_max(mx);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = mx;
   __syncthreads();
-  mx = fmaxf(red[0], red[1]);
+  mx = -INFINITY;
+  for (int i = 0; i < HD * kMergeGroups / 64; ++i) mx = fmaxf(mx, wmax[i]);
   float num = 0.f, den = 0.f;
-  if (d < HD) {
-#pragma unroll 8
-    for (int t = 0; t < n; ++t) {
-      const size_t item = static_cast<size_t>(s0 + t) * a.n_kv + kh;
-      const float ms = t < nc ? sm[t] : a.part_ml[item * 32 + c];
-      const float ls = t < nc ? sl[t] : a.part_ml[item * 32 + 16 + c];
-      const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
-      den += w * ls;
-      num += w * a.part_o[(item * 16 + c) * HD + d];
-    }
-    static_cast<bf16_t*>(a.out)[(static_cast<size_t>(b) * a.n_q + h) * HD + d] = f32_to_bf16(num / den);
+#pragma unroll 4
+  for (int t = q; t < n; t += kMergeGroups) {
+    const float ms = t < nc ? sm[t] : m_of(t);
+    const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
+    num += w * a.part_o[((static_cast<size_t>(s0 + t) * a.n_kv + kh) * 16 + c) * HD + d];
+    if (d == 0) den += w * (t < nc ? sl[t] : l_of(t));
+  }
+  part_num[q][d] = num;
+  if (d == 0) part_den[q] = den;
+  __syncthreads();
+  if (q == 0) {
+    float tn = 0.f, td = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMergeGroups; ++i) { tn += part_num[i][d]; td += part_den[i]; }
+    static_cast<bf16_t*>(a.out)[(static_cast<size_t>(b) * a.n_q + h) * HD + d] = f32_to_bf16(tn / td);
   }
 }
 
@@ -314,8 +324,8 @@ hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s) {
 hipError_t launch_attn_merge(const AttnArgs& a, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;
   dim3 grid(a.B, a.n_q);
-  if (a.hd == 128) hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(128), 0, s, a);
-  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_merge<64>, grid, dim3(128), 0, s, a);
+  if (a.hd == 128) hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(128 * kMergeGroups), 0, s, a);
+  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_merge<64>, grid, dim3(64 * kMergeGroups), 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -331,6 +331,14 @@ hipError_t launch_add_norm_t(const AddNormArgs& a, hipStream_t s) {
     case 6: launch_add_norm_s<T, 6>(a, th, s); break;
     case 7: launch_add_norm_s<T, 7>(a, th, s); break;
     case 8: launch_add_norm_s<T, 8>(a, th, s); break;
+    case 9: launch_add_norm_s<T, 9>(a, th, s); break;
+    case 10: launch_add_norm_s<T, 10>(a, th, s); break;
+    case 11: launch_add_norm_s<T, 11>(a, th, s); break;
+    case 12: launch_add_norm_s<T, 12>(a, th, s); break;
+    case 13: launch_add_norm_s<T, 13>(a, th, s); break;
+    case 14: launch_add_norm_s<T, 14>(a, th, s); break;
+    case 15: launch_add_norm_s<T, 15>(a, th, s); break;
+    case 16: launch_add_norm_s<T, 16>(a, th, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -349,6 +357,14 @@ hipError_t launch_rope_t(const RopeArgs& a, hipStream_t s) {
     case 6: hipLaunchKernelGGL((k_rope_append<T, 6>), grid, dim3(256), 0, s, a); break;
     case 7: hipLaunchKernelGGL((k_rope_append<T, 7>), grid, dim3(256), 0, s, a); break;
     case 8: hipLaunchKernelGGL((k_rope_append<T, 8>), grid, dim3(256), 0, s, a); break;
+    case 9: hipLaunchKernelGGL((k_rope_append<T, 9>), grid, dim3(256), 0, s, a); break;
+    case 10: hipLaunchKernelGGL((k_rope_append<T, 10>), grid, dim3(256), 0, s, a); break;
+    case 11: hipLaunchKernelGGL((k_rope_append<T, 11>), grid, dim3(256), 0, s, a); break;
+    case 12: hipLaunchKernelGGL((k_rope_append<T, 12>), grid, dim3(256), 0, s, a); break;
+    case 13: hipLaunchKernelGGL((k_rope_append<T, 13>), grid, dim3(256), 0, s, a); break;
+    case 14: hipLaunchKernelGGL((k_rope_append<T, 14>), grid, dim3(256), 0, s, a); break;
+    case 15: hipLaunchKernelGGL((k_rope_append<T, 15>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_rope_append<T, 16>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -20,6 +20,8 @@
 //
 // The SiLU epilogue pairs gate row i with up row i in one thread and writes
 // silu(gate) * up once, rounded to the storage type.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -46,19 +48,20 @@ __global__ __launch_bounds__(256) void k_gemm_stream(GemmArgs a, int chunks_per_
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, r = lane & 15;
   const int K = a.K;
+  const int bx = blockIdx.x, m0 = 0;
   const bf16_t* wrow[R];
 #pragma unroll
   for (int t = 0; t < R; ++t) {
     if (SILU) {
-      wrow[t] = static_cast<const bf16_t*>(a.W.ptr[t]) + static_cast<size_t>(blockIdx.x * 16 + r) * K;
+      wrow[t] = static_cast<const bf16_t*>(a.W.ptr[t]) + static_cast<size_t>(bx * 16 + r) * K;
     } else {
-      wrow[t] = seg_row<bf16_t>(a.W, (blockIdx.x * R + t) * 16 + r, K);
+      wrow[t] = seg_row<bf16_t>(a.W, (bx * R + t) * 16 + r, K);
     }
   }
   const bf16_t* arow[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    int m = mt * 16 + r;
+    int m = m0 + mt * 16 + r;
     if (m >= a.M) m = a.M - 1;
     arow[mt] = static_cast<const bf16_t*>(a.A) + static_cast<size_t>(m) * a.lda;
   }
@@ -117,10 +120,10 @@ __global__ __launch_bounds__(256) void k_gemm_stream(GemmArgs a, int chunks_per_
     for (int q = threadIdx.x; q < NSL * 64; q += 256) {
       const int ln = q & 63, sl = q >> 6;
       const int e = sl & 3, tm = sl >> 2, mt = tm % MT, t = tm / MT;
-      const int m = mt * 16 + (ln & 15);
+      const int m = m0 + mt * 16 + (ln & 15);
       if (m < a.M) {
         const float v = red[0][sl][ln] + red[1][sl][ln] + red[2][sl][ln] + red[3][sl][ln];
-        const int n = (blockIdx.x * R + t) * 16 + (ln >> 4) * 4 + e;
+        const int n = (bx * R + t) * 16 + (ln >> 4) * 4 + e;
         a.part[(static_cast<size_t>(blockIdx.y) * a.M + m) * a.N + n] = v;
       }
     }
@@ -129,13 +132,141 @@ __global__ __launch_bounds__(256) void k_gemm_stream(GemmArgs a, int chunks_per_
     for (int q = threadIdx.x; q < MT * 4 * 64; q += 256) {
       const int ln = q & 63, sl = q >> 6;
       const int e = sl & 3, mt = sl >> 2;
-      const int m = mt * 16 + (ln & 15);
+      const int m = m0 + mt * 16 + (ln & 15);
       if (m < a.M) {
         const int sg = mt * 4 + e, su = (MT + mt) * 4 + e;
         const float gv = red[0][sg][ln] + red[1][sg][ln] + red[2][sg][ln] + red[3][sg][ln];
         const float uv = red[0][su][ln] + red[1][su][ln] + red[2][su][ln] + red[3][su][ln];
-        const int i = blockIdx.x * 16 + (ln >> 4) * 4 + e;
+        const int i = bx * 16 + (ln >> 4) * 4 + e;
         out[static_cast<size_t>(m) * a.N + i] = f32_to_bf16(silu(gv) * uv);
+      }
+    }
+  }
+}
+
+// ---- decode-regime weight streaming with the activations shared in LDS ------
+// The 4 waves of a block own different weight rows and the same K range, so
+// each 128-wide activation chunk is fetched once per block into LDS (double
+// buffered) and read by all waves; weights stream into registers, double
+// buffered.  Wave w owns rows (blockIdx.x*4 + w)*16R .. +16R, or, with the
+// SiLU epilogue, output indices (blockIdx.x*4 + w)*16 .. +16 (gate and up).
+constexpr int kSkLd = 128 + 8;  // padded LDS row of one activation chunk (elements)
+
+template <int R, int MT, bool SILU>
+__global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a, int chunks_per_split) {
+  constexpr int AROWS = MT * 16;
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][AROWS * kSkLd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r = lane & 15;
+  const int K = a.K;
+  const int unit = blockIdx.x * 4 + wave;
+  const bf16_t* wrow[R];
+#pragma unroll
+  for (int t = 0; t < R; ++t) {
+    if (SILU) wrow[t] = static_cast<const bf16_t*>(a.W.ptr[t]) + static_cast<size_t>(unit * 16 + r) * K;
+    else wrow[t] = seg_row<bf16_t>(a.W, (unit * R + t) * 16 + r, K);
+  }
+  // activation chunk loader: AROWS rows x 16 pieces of 16 bytes, MT pieces per thread
+  const bf16_t* asrc[MT];
+  int aoff[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int q = tid + 256 * i;
+    const int row = q >> 4, col = (q & 15) * 8;
+    int m = row < a.M ? row : a.M - 1;
+    asrc[i] = static_cast<const bf16_t*>(a.A) + static_cast<size_t>(m) * a.lda + col;
+    aoff[i] = row * kSkLd + col;
+  }
+  f32x4_t acc[R][MT];
+#pragma unroll
+  for (int t = 0; t < R; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  bf16x8_t wv[2][R][4];
+  uint4 areg[MT];
+  auto load_w = [&](int buf, int chunk) {
+    const int k = chunk * 128 + g * 32;
+#pragma unroll
+    for (int t = 0; t < R; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) wv[buf][t][j] = load_bf16x8(wrow[t] + k + 8 * j);
+  };
+  auto load_a = [&](int chunk) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) areg[i] = *reinterpret_cast<const uint4*>(asrc[i] + chunk * 128);
+  };
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) *reinterpret_cast<uint4*>(&As[buf][aoff[i]]) = areg[i];
+  };
+  auto compute = [&](int wbuf, int abuf) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      bf16x8_t af[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) af[mt] = load_bf16x8(&As[abuf][(mt * 16 + r) * kSkLd + g * 32 + j * 8]);
+#pragma unroll
+      for (int t = 0; t < R; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] = mfma16x16x32(wv[wbuf][t][j], af[mt], acc[t][mt]);
+    }
+  };
+
+  const int n_chunks = K / 128;
+  const int c0 = blockIdx.y * chunks_per_split;
+  const int c1 = min(c0 + chunks_per_split, n_chunks);
+  // Vector-memory loads complete in issue order, so the next activation
+  // chunk is issued before the next weight chunk: storing it to LDS at the end
+  // of the step then waits only for the activations (an L2 hit), never for
+  // weights still in flight from HBM.
+  if (c0 < c1) {
+    load_a(c0);
+    load_w(0, c0);
+    store_a(0);
+  }
+  __syncthreads();
+  for (int c = c0; c < c1; c += 2) {
+    // even step: W buffer 0, A buffer 0
+    if (c + 1 < c1) {
+      load_a(c + 1);
+      asm volatile("" ::: "memory");
+      load_w(1, c + 1);
+    }
+    compute(0, 0);
+    if (c + 1 < c1) store_a(1);
+    __syncthreads();
+    if (c + 1 >= c1) break;
+    // odd step: W buffer 1, A buffer 1
+    if (c + 2 < c1) {
+      load_a(c + 2);
+      asm volatile("" ::: "memory");
+      load_w(0, c + 2);
+    }
+    compute(1, 1);
+    if (c + 2 < c1) store_a(0);
+    __syncthreads();
+  }
+
+  // lane (g, c) holds C^T[row base + t*16 + 4g + e][m = mt*16 + c]
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = mt * 16 + r;
+    if (m >= a.M) continue;
+    if (SILU) {
+      const int i0 = unit * 16 + g * 4;
+      uint2 pk;
+      pk.x = static_cast<uint32_t>(f32_to_bf16(silu(acc[0][mt][0]) * acc[1][mt][0])) |
+             (static_cast<uint32_t>(f32_to_bf16(silu(acc[0][mt][1]) * acc[1][mt][1])) << 16);
+      pk.y = static_cast<uint32_t>(f32_to_bf16(silu(acc[0][mt][2]) * acc[1][mt][2])) |
+             (static_cast<uint32_t>(f32_to_bf16(silu(acc[0][mt][3]) * acc[1][mt][3])) << 16);
+      *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.act_out) + static_cast<size_t>(m) * a.N + i0) = pk;
+    } else {
+#pragma unroll
+      for (int t = 0; t < R; ++t) {
+        const int n = (unit * R + t) * 16 + g * 4;
+        *reinterpret_cast<float4*>(a.part + (static_cast<size_t>(blockIdx.y) * a.M + m) * a.N + n) =
+            make_float4(acc[t][mt][0], acc[t][mt][1], acc[t][mt][2], acc[t][mt][3]);
       }
     }
   }
@@ -325,8 +456,7 @@ void launch_stream_t(const GemmArgs& a, hipStream_t s) {
 
 template <bool SILU>
 void launch_stream_m(const GemmArgs& a, hipStream_t s) {
-  const int mt = (a.M + 15) / 16;
-  switch (mt) {
+  switch ((a.M + 15) / 16) {
     case 1: launch_stream_t<2, 1, SILU>(a, s); break;
     case 2: launch_stream_t<2, 2, SILU>(a, s); break;
     case 3: launch_stream_t<2, 3, SILU>(a, s); break;
@@ -334,45 +464,116 @@ void launch_stream_m(const GemmArgs& a, hipStream_t s) {
   }
 }
 
+template <int R, int MT, bool SILU>
+void launch_skinny_t(const GemmArgs& a, hipStream_t s) {
+  const int n_chunks = a.K / 128;
+  const int cps = (n_chunks + a.splits - 1) / a.splits;
+  const int blocks = SILU ? a.N / 64 : a.N / (64 * R);
+  hipLaunchKernelGGL((k_gemm_skinny<R, MT, SILU>), dim3(blocks, a.splits), dim3(256), 0, s, a, cps);
+}
+
+template <int R, bool SILU>
+void launch_skinny_m(const GemmArgs& a, hipStream_t s) {
+  switch ((a.M + 15) / 16) {
+    case 1: launch_skinny_t<R, 1, SILU>(a, s); break;
+    case 2: launch_skinny_t<R, 2, SILU>(a, s); break;
+    case 3: launch_skinny_t<R, 3, SILU>(a, s); break;
+    default: launch_skinny_t<R, 4, SILU>(a, s); break;
+  }
+}
+
+enum GemmKernel { kKStream = 1, kKSkinny16 = 2, kKSkinny32 = 3, kKTiled = 4, kKF32 = 5 };
+
+struct GemmPlan {
+  int kernel;
+  int splits;
+};
+
+// Number of K splits that leaves no split empty, for a wish of `want`.
+int even_splits(int n_units, int want) {
+  if (want < 1) want = 1;
+  if (want > n_units) want = n_units;
+  const int per = (n_units + want - 1) / want;
+  return (n_units + per - 1) / per;
+}
+
+// Kernel and split choice, from sweeps of the Qwen2.5 decode shapes on
+// gfx950: per-wave activation loads win for the wide gate/up projection and
+// for the LM head at tiny batches; LDS-shared activations with 16 (M <= 16)
+// or 32 (M > 16) weight rows per wave win elsewhere; the K split is the
+// smallest that gives roughly two blocks per CU.
+GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
+  if (!bf16) return {kKF32, 1};
+  if (M > 64) {
+    const int blocks = (silu ? N / 64 : N / kTBN) * ((M + kTBM - 1) / kTBM);
+    int s = silu ? 1 : (512 + blocks - 1) / blocks;
+    s = std::min(s, std::max(1, (K / kTBK) / 4));
+    return {kKTiled, even_splits(K / kTBK, std::min(s, max_splits))};
+  }
+  const int n_chunks = K / 128;
+  auto pick = [&](int blocks, int target) {
+    int s = 1;
+    for (int c : {1, 2, 3, 4, 6, 8, 12, 16}) {
+      s = c;
+      if (blocks * c >= target) break;
+    }
+    s = std::min(std::min(s, max_splits), std::max(1, n_chunks / 2));
+    return even_splits(n_chunks, s);
+  };
+  if (silu) return {kKStream, 1};
+  if (M <= 16) {
+    if (N >= 16384) return {M <= 8 ? kKStream : kKSkinny32, 1};
+    return {kKSkinny16, pick(N / 64, 512)};
+  }
+  return {kKSkinny32, pick(N / 128, K >= 8192 ? 448 : 256)};
+}
+
 }  // namespace
 
-int gemm_pick_splits(int bf16, int M, int N, int K, int max_splits) {
-  if (!bf16) return 1;
-  int blocks, max_by_k;
-  if (M <= 64) {
-    blocks = N / 32;
-    max_by_k = (K / 128) / 4;  // at least one chunk per wave
-  } else {
-    blocks = (N / kTBN) * ((M + kTBM - 1) / kTBM);
-    max_by_k = (K / kTBK) / 4;
-  }
-  int s = (512 + blocks - 1) / blocks;
-  if (s > max_by_k) s = max_by_k;
-  if (s > max_splits) s = max_splits;
-  return s < 1 ? 1 : s;
+int gemm_pick_splits(int bf16, int M, int N, int K, bool silu, int max_splits) {
+  return plan_gemm(bf16, M, N, K, silu, max_splits).splits;
 }
 
 hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (a.splits < 1 || (a.epi == kEpiSiluMul && a.splits != 1)) return hipErrorInvalidValue;
-  if (!bf16) {
-    if (a.splits != 1) return hipErrorInvalidValue;
+  const bool silu = a.epi == kEpiSiluMul;
+  if (a.splits < 1 || (silu && a.splits != 1)) return hipErrorInvalidValue;
+  const int kernel = a.variant ? a.variant : plan_gemm(bf16, a.M, a.N, a.K, silu, 64).kernel;
+  if (!bf16 || kernel == kKF32) {
+    if (bf16 || a.splits != 1) return hipErrorInvalidValue;
     dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
-    if (a.epi == kEpiSiluMul) hipLaunchKernelGGL(k_gemm_f32<true>, grid, dim3(256), 0, s, a);
+    if (silu) hipLaunchKernelGGL(k_gemm_f32<true>, grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL(k_gemm_f32<false>, grid, dim3(256), 0, s, a);
     return hipGetLastError();
   }
-  if (a.M <= 64) {
-    if (a.K % 128 != 0 || a.N % (a.epi == kEpiSiluMul ? 16 : 32) != 0) return hipErrorInvalidValue;
-    if (a.epi == kEpiSiluMul) launch_stream_m<true>(a, s);
-    else launch_stream_m<false>(a, s);
-  } else {
-    if (a.K % kTBK != 0 || a.N % (a.epi == kEpiSiluMul ? 64 : kTBN) != 0) return hipErrorInvalidValue;
+  if (kernel == kKTiled || a.M > 64) {
+    if (a.K % kTBK != 0 || a.N % (silu ? 64 : kTBN) != 0) return hipErrorInvalidValue;
     const int kbps = (a.K / kTBK + a.splits - 1) / a.splits;
-    const int nb = a.epi == kEpiSiluMul ? a.N / 64 : a.N / kTBN;
+    const int nb = silu ? a.N / 64 : a.N / kTBN;
     dim3 grid(nb, (a.M + kTBM - 1) / kTBM, a.splits);
-    if (a.epi == kEpiSiluMul) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps);
+    if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps);
     else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(256), 0, s, a, kbps);
+    return hipGetLastError();
+  }
+  if (a.K % 128 != 0) return hipErrorInvalidValue;
+  switch (kernel) {
+    case kKStream:
+      if (a.N % (silu ? 16 : 32) != 0) return hipErrorInvalidValue;
+      if (silu) launch_stream_m<true>(a, s);
+      else launch_stream_m<false>(a, s);
+      break;
+    case kKSkinny16:
+      if (a.N % 64 != 0) return hipErrorInvalidValue;
+      if (silu) launch_skinny_m<2, true>(a, s);
+      else launch_skinny_m<1, false>(a, s);
+      break;
+    case kKSkinny32:
+      if (a.N % (silu ? 64 : 128) != 0) return hipErrorInvalidValue;
+      if (silu) launch_skinny_m<2, true>(a, s);
+      else launch_skinny_m<2, false>(a, s);
+      break;
+    default:
+      return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

@@ -36,12 +36,13 @@ struct GemmArgs {
   int splits;        // S >= 1; kEpiSiluMul requires 1
   float* part;       // [S, M, N] (kEpiPartial)
   void* act_out;     // [M, N] dtype T (kEpiSiluMul)
+  int variant;       // 0: automatic; 1 stream, 2/3 skinny (16/32 rows per wave), 4 tiled
 };
 
-// Picks the kernel from dtype and M.  Returns hipSuccess or a launch error.
+// Picks the kernel from dtype, M, N and K.  Returns hipSuccess or a launch error.
 hipError_t launch_gemm(int dtype_bf16, const GemmArgs& a, hipStream_t s);
-// Split count the launcher would like for this shape (1 = none).
-int gemm_pick_splits(int dtype_bf16, int M, int N, int K, int max_splits);
+// K-split count the launcher plans for this shape (1 = none, never an empty split).
+int gemm_pick_splits(int dtype_bf16, int M, int N, int K, bool silu, int max_splits);
 
 struct EmbedArgs {
   const void* embed; const void* norm_g;
