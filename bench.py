@@ -121,6 +121,9 @@ def main():
     ap.add_argument("--kernel", default="gemm_gate_up", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--max-prefill-tokens", type=int, default=16384)
+    ap.add_argument("--compare-unscheduled", action="store_true",
+                    help="after the timed steps, run the same sequences as one unscheduled batch and report "
+                         "both schedules (meaningful for 7b-mixed: short round + long round vs one batch)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -207,6 +210,18 @@ def main():
                    "rounds": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in s.items()} for s in last]},
         "roofline": roof,
     }
+    if args.compare_unscheduled and wl.round_id is not None:
+        log("running the same sequences as one unscheduled batch")
+        _, flat = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, wl.sample_seed,
+                              wl.temperature, None)
+        sched_make = sum(s_["makespan_ms"] for s_ in last) / 1e3
+        sched_idle = sum(s_["idle_slot_s"] for s_ in last)
+        out["config"]["schedule_comparison"] = {
+            "rounds_makespan_s": round(sched_make, 3), "rounds_idle_slot_s": round(sched_idle, 1),
+            "unscheduled_makespan_s": round(flat[0]["makespan_ms"] / 1e3, 3),
+            "unscheduled_idle_slot_s": round(flat[0]["idle_slot_s"], 1),
+            "unscheduled_slot_idle": round(flat[0]["slot_idle"], 4),
+            "idle_reduction": round(flat[0]["idle_slot_s"] / max(sched_idle, 1e-9), 3)}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(weights, shape, wl)

@@ -273,109 +273,140 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a, int chunks_per_
 }
 
 // ---- prefill / large-batch tiled MFMA GEMM ---------------------------------
-constexpr int kTBN = 128, kTBM = 128, kTBK = 64, kTLDK = kTBK + 8;
+// Block tile: 128 activation rows (m) x 256 weight rows (n), K step 64, four
+// waves as 2 (m) x 2 (n), each computing 64 m x 128 n with
+// v_mfma_f32_32x32x16_bf16 (2 x 4 tiles, 128 fp32 accumulators per lane).
+// Activations are the MFMA row operand and weights the column operand, so
+// the 32 lanes of one accumulator register hold 32 consecutive n: coalesced
+// stores.  Two padded LDS stages; the next K step is prefetched into
+// registers while the current one is multiplied; one barrier per K step.
+// Tiles are ordered so that the blocks an XCD runs back to back (ids equal
+// mod 8) walk the m tiles of one weight panel, which then stays in that
+// XCD's L2.
+constexpr int kGBM = 128, kGBN = 256, kGBK = 64, kGLD = kGBK + 8;
 
 template <bool SILU>
-__global__ __launch_bounds__(256) void k_gemm_tiled(GemmArgs a, int kblocks_per_split) {
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[kTBN * kTLDK];
-  __shared__ __attribute__((aligned(16))) bf16_t As[kTBM * kTLDK];
+__global__ __launch_bounds__(256) void k_gemm_tiled(GemmArgs a, int kblocks_per_split, int n_mb, int n_nb) {
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][kGBM * kGLD];
+  __shared__ __attribute__((aligned(16))) bf16_t Ws[2][kGBN * kGLD];
+  const int n_tiles = n_mb * n_nb;
+  const int per_xcd = (n_tiles + 7) / 8;
+  const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (t >= n_tiles) return;  // block-uniform: padding of the XCD-ordered grid
+  const int nb = t / n_mb, mb = t % n_mb;
+  const int split = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane >> 4, r = lane & 15;
-  const int wn = wave & 1, wm = wave >> 1;
-  const int bn = blockIdx.x, bm = blockIdx.y, split = blockIdx.z;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int l32 = lane & 31, lh = lane >> 5;
   const int K = a.K;
 
-  const bf16_t* wsrc[4];
+  // global -> LDS assignment: A 128 rows x 8 pieces (4 per thread), W 256 rows x 8 pieces (8 per thread)
   const bf16_t* asrc[4];
-  int lds_off[4];
+  const bf16_t* wsrc[8];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int q = tid + 256 * i;
-    const int row = q >> 3, col = (q & 7) * 8;
-    if (SILU) {
-      const int tt = row >> 4, rr = row & 15;
-      const int idx = bn * 64 + (tt >> 1) * 16 + rr;
-      wsrc[i] = static_cast<const bf16_t*>(a.W.ptr[tt & 1]) + static_cast<size_t>(idx) * K + col;
-    } else {
-      wsrc[i] = seg_row<bf16_t>(a.W, bn * kTBN + row, K) + col;
-    }
-    int m = bm * kTBM + row;
+    const int q = tid + 256 * i, row = q >> 3, col = (q & 7) * 8;
+    int m = mb * kGBM + row;
     if (m >= a.M) m = a.M - 1;
     asrc[i] = static_cast<const bf16_t*>(a.A) + static_cast<size_t>(m) * a.lda + col;
-    lds_off[i] = row * kTLDK + col;
   }
-
-  f32x4_t acc[4][4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int i = 0; i < 8; ++i) {
+    const int q = tid + 256 * i, row = q >> 3, col = (q & 7) * 8;
+    if (SILU) {
+      const int grp = row >> 5;  // 32-row groups alternate gate / up over the same indices
+      const int idx = nb * 128 + (grp >> 1) * 32 + (row & 31);
+      wsrc[i] = static_cast<const bf16_t*>(a.W.ptr[grp & 1]) + static_cast<size_t>(idx) * K + col;
+    } else {
+      int n = nb * kGBN + row;
+      if (n >= a.N) n = a.N - 1;
+      wsrc[i] = seg_row<bf16_t>(a.W, n, K) + col;
+    }
+  }
+  f32x16_t acc[2][4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc[t][u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[mt][nt][e] = 0.f;
 
   const int kb0 = split * kblocks_per_split;
-  const int kb1 = min(kb0 + kblocks_per_split, K / kTBK);
-  uint4 wreg[4], areg[4];
+  const int kb1 = min(kb0 + kblocks_per_split, K / kGBK);
+  uint4 ra[4], rw[8];
+  auto load = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ra[i] = *reinterpret_cast<const uint4*>(asrc[i] + kb * kGBK);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) rw[i] = *reinterpret_cast<const uint4*>(wsrc[i] + kb * kGBK);
+  };
+  auto store = [&](int st) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int q = tid + 256 * i;
+      *reinterpret_cast<uint4*>(&As[st][(q >> 3) * kGLD + (q & 7) * 8]) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int q = tid + 256 * i;
+      *reinterpret_cast<uint4*>(&Ws[st][(q >> 3) * kGLD + (q & 7) * 8]) = rw[i];
+    }
+  };
+  auto compute = [&](int st) {
+#pragma unroll
+    for (int kk = 0; kk < kGBK; kk += 16) {
+      bf16x8_t af[2], bw[4];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) af[mt] = load_bf16x8(&As[st][(wm * 64 + mt * 32 + l32) * kGLD + kk + 8 * lh]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) bw[nt] = load_bf16x8(&Ws[st][(wn * 128 + nt * 32 + l32) * kGLD + kk + 8 * lh]);
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma32x32x16(af[mt], bw[nt], acc[mt][nt]);
+    }
+  };
   if (kb0 < kb1) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      wreg[i] = *reinterpret_cast<const uint4*>(wsrc[i] + kb0 * kTBK);
-      areg[i] = *reinterpret_cast<const uint4*>(asrc[i] + kb0 * kTBK);
-    }
+    load(kb0);
+    store(0);
+    if (kb0 + 1 < kb1) load(kb0 + 1);
   }
-  for (int kb = kb0; kb < kb1; ++kb) {
+  __syncthreads();
+  for (int kb = kb0; kb < kb1; kb += 2) {
+    compute(0);
+    if (kb + 1 < kb1) store(1);
+    if (kb + 2 < kb1) load(kb + 2);
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(&Ws[lds_off[i]]) = wreg[i];
-      *reinterpret_cast<uint4*>(&As[lds_off[i]]) = areg[i];
-    }
+    if (kb + 1 >= kb1) break;
+    compute(1);
+    if (kb + 2 < kb1) store(0);
+    if (kb + 3 < kb1) load(kb + 3);
     __syncthreads();
-    if (kb + 1 < kb1) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        wreg[i] = *reinterpret_cast<const uint4*>(wsrc[i] + (kb + 1) * kTBK);
-        areg[i] = *reinterpret_cast<const uint4*>(asrc[i] + (kb + 1) * kTBK);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < kTBK; kk += 32) {
-      bf16x8_t af[4], bfr[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) af[t] = load_bf16x8(&Ws[(wn * 64 + t * 16 + r) * kTLDK + kk + g * 8]);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) bfr[u] = load_bf16x8(&As[(wm * 64 + u * 16 + r) * kTLDK + kk + g * 8]);
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) acc[t][u] = mfma16x16x32(af[t], bfr[u], acc[t][u]);
-    }
   }
 
-  // lane (g, c) holds C^T[n = wn*64 + t*16 + 4g + e][m = wm*64 + u*16 + c]
+  // acc[mt][nt] register e: m = wm*64 + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*128 + nt*32 + l32
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int m = bm * kTBM + wm * 64 + u * 16 + r;
-    if (m >= a.M) continue;
-    if (SILU) {
-      bf16_t* out = static_cast<bf16_t*>(a.act_out);
+  for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int i0 = bn * 64 + (wn * 2 + p) * 16 + g * 4;
-        uint2 pk;
-        pk.x = static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][0]) * acc[2 * p + 1][u][0])) |
-               (static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][1]) * acc[2 * p + 1][u][1])) << 16);
-        pk.y = static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][2]) * acc[2 * p + 1][u][2])) |
-               (static_cast<uint32_t>(f32_to_bf16(silu(acc[2 * p][u][3]) * acc[2 * p + 1][u][3])) << 16);
-        *reinterpret_cast<uint2*>(out + static_cast<size_t>(m) * a.N + i0) = pk;
-      }
-    } else {
+    for (int e = 0; e < 16; ++e) {
+      const int m = mb * kGBM + wm * 64 + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+      if (m >= a.M) continue;
+      if (SILU) {
+        bf16_t* out = static_cast<bf16_t*>(a.act_out) + static_cast<size_t>(m) * a.N;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int n = bn * kTBN + wn * 64 + t * 16 + g * 4;
-        float4 v = make_float4(acc[t][u][0], acc[t][u][1], acc[t][u][2], acc[t][u][3]);
-        *reinterpret_cast<float4*>(a.part + (static_cast<size_t>(split) * a.M + m) * a.N + n) = v;
+        for (int p = 0; p < 2; ++p) {
+          const int idx = nb * 128 + (wn * 2 + p) * 32 + l32;
+          out[idx] = f32_to_bf16(silu(acc[mt][2 * p][e]) * acc[mt][2 * p + 1][e]);
+        }
+      } else {
+        float* out = a.part + (static_cast<size_t>(split) * a.M + m) * a.N;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          const int n = nb * kGBN + wn * 128 + nt * 32 + l32;
+          if (n < a.N) out[n] = acc[mt][nt][e];
+        }
       }
     }
-  }
 }
 
 // ---- fp32 model ------------------------------------------------------------
@@ -505,10 +536,10 @@ int even_splits(int n_units, int want) {
 GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
   if (!bf16) return {kKF32, 1};
   if (M > 64) {
-    const int blocks = (silu ? N / 64 : N / kTBN) * ((M + kTBM - 1) / kTBM);
-    int s = silu ? 1 : (512 + blocks - 1) / blocks;
-    s = std::min(s, std::max(1, (K / kTBK) / 4));
-    return {kKTiled, even_splits(K / kTBK, std::min(s, max_splits))};
+    const int blocks = (silu ? N / 128 : (N + kGBN - 1) / kGBN) * ((M + kGBM - 1) / kGBM);
+    int s = silu ? 1 : (256 + blocks - 1) / blocks;
+    s = std::min(s, std::max(1, (K / kGBK) / 4));
+    return {kKTiled, even_splits(K / kGBK, std::min(s, max_splits))};
   }
   const int n_chunks = K / 128;
   auto pick = [&](int blocks, int target) {
@@ -547,12 +578,14 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   if (kernel == kKTiled || a.M > 64) {
-    if (a.K % kTBK != 0 || a.N % (silu ? 64 : kTBN) != 0) return hipErrorInvalidValue;
-    const int kbps = (a.K / kTBK + a.splits - 1) / a.splits;
-    const int nb = silu ? a.N / 64 : a.N / kTBN;
-    dim3 grid(nb, (a.M + kTBM - 1) / kTBM, a.splits);
-    if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps);
-    else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(256), 0, s, a, kbps);
+    if (a.K % kGBK != 0 || (silu && a.N % 128 != 0) || (!silu && a.N % 32 != 0)) return hipErrorInvalidValue;
+    const int kbps = (a.K / kGBK + a.splits - 1) / a.splits;
+    const int n_nb = silu ? a.N / 128 : (a.N + kGBN - 1) / kGBN;
+    const int n_mb = (a.M + kGBM - 1) / kGBM;
+    const int per_xcd = (n_mb * n_nb + 7) / 8;
+    dim3 grid(8 * per_xcd, a.splits);
+    if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps, n_mb, n_nb);
+    else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(256), 0, s, a, kbps, n_mb, n_nb);
     return hipGetLastError();
   }
   if (a.K % 128 != 0) return hipErrorInvalidValue;

@@ -182,6 +182,30 @@ def test_generate_with_sampler_is_reproducible(tiny):
     assert np.array_equal(a, b) and not np.array_equal(a, c)
 
 
+def test_bf16_round_matches_torch():
+    """The diagnostic rounding equals torch's fp32 -> bfloat16 conversion (round to nearest even)."""
+    rng = np.random.default_rng(11)
+    x = np.concatenate([rng.standard_normal(10000) * 10.0 ** rng.integers(-6, 6, 10000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.01171875, 3.0e38, -2.5e-38]])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(om.bf16_round(x), ref)
+
+
+def test_rounding_diagnostic_reduces_to_plain_oracle(tiny):
+    """rnd=None and rnd=identity give the plain fp64 forward; bf16 rounding stays close to it."""
+    s, w = tiny
+    toks = np.random.default_rng(12).integers(0, s.vocab, size=30)
+    plain = om.forward_full(w, s, toks)
+    ident = om.forward_full(w, s, toks, rnd=lambda v: v)      # same maths, P normalised after P @ V
+    assert np.max(np.abs(ident - plain)) < 1e-12
+    rounded = om.forward_full(w, s, toks, rnd=om.bf16_round)
+    err = np.max(np.abs(rounded - plain)) / np.max(np.abs(plain))
+    assert 1e-6 < err < 5e-2
+    st = om.KVState(s, om.bf16_round)
+    inc = np.concatenate([st.step(w, toks[:20]), st.step(w, toks[20:21]), st.step(w, toks[21:])])
+    assert np.max(np.abs(inc - rounded)) < 1e-10
+
+
 def test_truncated_shape_keeps_layer_dims():
     s = truncated(SHAPES["qwen2.5-7b"], 2)
     assert s.layers == 2 and s.hidden == 3584 and s.group == 7
