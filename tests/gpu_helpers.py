@@ -42,12 +42,12 @@ class ParityResult:
     worst: tuple
 
 
-def oracle_rollout(w64, shape, prompt, n_new, temperature, seed, seq_id):
+def oracle_rollout(w64, shape, prompt, n_new, temperature, seed, seq_id, rnd=None):
     sample_fn = osm.sampler(temperature, seed, seq_id)
-    return om.generate(w64, shape, prompt, n_new, sample_fn)
+    return om.generate(w64, shape, prompt, n_new, sample_fn, rnd)
 
 
-def teacher_forced_parity(eng, shape, w64, wl, n_new, tol, temperature, seed):
+def teacher_forced_parity(eng, shape, w64, wl, n_new, tol, temperature, seed, rnd=None):
     """Prefill + (n_new - 1) teacher-forced decode steps on the GPU vs the oracle.
 
     Per position r: e_r = max|l_gpu - l_ref| / max|l_ref|; the GPU's sampled
@@ -56,7 +56,7 @@ def teacher_forced_parity(eng, shape, w64, wl, n_new, tol, temperature, seed):
     """
     import torch
     n = wl.n
-    refs = [oracle_rollout(w64, shape, wl.prompt(i), n_new, temperature, seed, int(wl.seq_ids[i]))
+    refs = [oracle_rollout(w64, shape, wl.prompt(i), n_new, temperature, seed, int(wl.seq_ids[i]), rnd)
             for i in range(n)]
     ref_tok = np.stack([r[0] for r in refs])          # [n, n_new]
     ref_log = np.stack([r[1] for r in refs])          # [n, n_new, V]
