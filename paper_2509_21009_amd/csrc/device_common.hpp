@@ -65,6 +65,18 @@ __device__ __forceinline__ bf16x8_t load_bf16x8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
+// Raw buffer resource over `bytes` bytes at p: loads at byte offsets at or
+// past `bytes` return zeros instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0), static_cast<int>(bytes),
+                                           0x00020000);
+}
+
+// 16 bytes of bf16 at byte offset `off` of a buffer resource.
+__device__ __forceinline__ bf16x8_t load_bf16x8(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
 __device__ __forceinline__ f32x16_t mfma32x32x16(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }

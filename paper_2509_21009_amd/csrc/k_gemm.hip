@@ -6,7 +6,14 @@
 // accumulation and W as the 16-row "A" operand, activations as the
 // 16-column "B" operand, so one MFMA yields a [16 n, 16 m] tile of C^T.
 //
-//  * k_gemm_stream (M <= 64, the decode regime): the weights are streamed
+//  * k_gemm_deep (M <= 64, the decode regime, most shapes): weights stream
+//    from HBM through buffer loads into a ring of register stages; a stage
+//    is a 64-wide K unit in which each lane reads 32 contiguous bytes of a
+//    row, so one wave's two back-to-back loads cover the row's whole
+//    128-byte line.  Activations (L2-resident) are loaded one stage ahead
+//    into a single buffer.  The block's 4 waves take interleaved K units and
+//    reduce through LDS; blockIdx.y splits K further (fp32 partials).
+//  * k_gemm_stream (M <= 64, the remaining decode shapes): the weights are streamed
 //    once from HBM straight into registers; every lane loads 64 contiguous
 //    bytes per row per 128-wide K chunk (the K order inside a chunk is
 //    permuted identically for both operands, which leaves the dot products
@@ -272,6 +279,174 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a, int chunks_per_
   }
 }
 
+// ---- decode-regime weight streaming, deep register pipeline ----------------
+// Block: 4 waves on the same 16R weight rows (with the SiLU epilogue: R/2
+// gate fragments and the R/2 up fragments of the same output indices).
+// A stage is a 64-wide K unit: lane (g, r) loads bytes [32g, 32g + 32) of
+// the unit's 128 bytes of row r as two 16-byte loads, and MFMA k-step j of
+// the unit takes the j-th of them from both operands, so every product of
+// the unit is formed exactly once.  Wave w takes units w, w + 4, ... of the
+// block's K range, so the block reads whole 512-byte runs of each row.
+// Weight fragments use one buffer resource each: rows past the end of the
+// matrix (the ragged last block) read as zeros and are never stored.
+template <int R, int MT, int D, bool SILU>
+__global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_split) {
+  static_assert(!SILU || R % 2 == 0, "SiLU pairs gate and up fragments");
+  constexpr int NACC = R * MT;
+  __shared__ __attribute__((aligned(16))) f32x4_t red[3][NACC][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  const int K = a.K, KU = K / 64;
+  const int u0 = blockIdx.y * units_per_split;
+  const int u1 = min(u0 + units_per_split, KU);
+  const int nblk = max(u1 - u0, 0);
+  const int nk = nblk > wave ? (nblk - wave + 3) / 4 : 0;
+  const uint32_t row_bytes = static_cast<uint32_t>(K) * 2u;
+
+  __amdgpu_buffer_rsrc_t rw[R];
+#pragma unroll
+  for (int t = 0; t < R; ++t) {
+    const bf16_t* base;
+    int valid;
+    if (SILU) {
+      const int row0 = (blockIdx.x * (R / 2) + t % (R / 2)) * 16;
+      valid = row0 < a.N ? min(16, a.N - row0) : 0;
+      base = static_cast<const bf16_t*>(a.W.ptr[t / (R / 2)]) + static_cast<size_t>(valid ? row0 : 0) * K;
+    } else {
+      const int row0 = (blockIdx.x * R + t) * 16;
+      int b = 0, sg = 0;
+      while (sg < a.W.n_seg - 1 && row0 >= b + a.W.rows[sg]) b += a.W.rows[sg++];
+      valid = row0 < a.N ? min(16, a.W.rows[sg] - (row0 - b)) : 0;
+      base = static_cast<const bf16_t*>(a.W.ptr[sg]) + static_cast<size_t>(valid ? row0 - b : 0) * K;
+    }
+    rw[t] = buffer_rsrc(base, static_cast<uint32_t>(valid) * row_bytes);
+  }
+  // rows m >= M of the activations read as zeros
+  const __amdgpu_buffer_rsrc_t ra =
+      buffer_rsrc(a.A, static_cast<uint32_t>(a.M) * static_cast<uint32_t>(a.lda) * 2u);
+  const int kb = (u0 + wave) * 128 + g * 32;
+  const int woff = r * static_cast<int>(row_bytes) + kb;
+  int aoff[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) aoff[mt] = (mt * 16 + r) * static_cast<int>(a.lda) * 2 + kb;
+
+  f32x4_t acc[R][MT];
+#pragma unroll
+  for (int t = 0; t < R; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // Weights: a ring of D stages.  Activations: one buffer, loaded one stage
+  // ahead, after the weights of the current stage and before those of later
+  // stages; vector loads complete in issue order, so waiting for the
+  // activations of stage s never waits for weights of later stages.
+  bf16x8_t wv[D][R][2], av[MT][2];
+  auto load_w = [&](int s, int unit) {
+    const int o = unit * 512;
+#pragma unroll
+    for (int t = 0; t < R; ++t) {
+      wv[s][t][0] = load_bf16x8(rw[t], woff + o);
+      wv[s][t][1] = load_bf16x8(rw[t], woff + o + 16);
+    }
+  };
+  auto load_a = [&](int unit) {
+    const int o = unit * 512;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      av[mt][0] = load_bf16x8(ra, aoff[mt] + o);
+      av[mt][1] = load_bf16x8(ra, aoff[mt] + o + 16);
+    }
+  };
+  auto compute = [&](int s) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int t = 0; t < R; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] = mfma16x16x32(wv[s][t][j], av[mt][j], acc[t][mt]);
+  };
+
+  // The prologue loads unconditionally (stages past the wave's range are
+  // in bounds and never used) and the scheduling barriers keep the issue
+  // order, so every path into the main loop has the same loads in flight and
+  // the compiler's wait counts there are exact.
+  load_w(0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  load_a(0);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int s = 1; s < D; ++s) {
+    load_w(s, s);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  int i = 0;
+  for (; i + 2 * D <= nk; i += D) {
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+      compute(s);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(i + s + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      load_w(s, i + s + D);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 2 * D; ++j) {
+    if (i + j < nk) {
+      compute(j % D);
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + j + 1 < nk) load_a(i + j + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + j + D < nk) load_w(j % D, i + j + D);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  if (wave > 0) {
+#pragma unroll
+    for (int t = 0; t < R; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) red[wave - 1][t * MT + mt][lane] = acc[t][mt];
+  }
+  __syncthreads();
+  if (wave > 0) return;
+#pragma unroll
+  for (int t = 0; t < R; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+      acc[t][mt] = acc[t][mt] + red[0][t * MT + mt][lane] + red[1][t * MT + mt][lane] + red[2][t * MT + mt][lane];
+
+  // lane (g, r) holds C^T[row base + t*16 + 4g + e][m = mt*16 + r]
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = mt * 16 + r;
+    if (m >= a.M) continue;
+    if (SILU) {
+#pragma unroll
+      for (int t = 0; t < R / 2; ++t) {
+        const int i0 = (blockIdx.x * (R / 2) + t) * 16 + g * 4;
+        if (i0 >= a.N) continue;
+        const f32x4_t gv = acc[t][mt], uv = acc[t + R / 2][mt];
+        uint2 pk;
+        pk.x = static_cast<uint32_t>(f32_to_bf16(silu(gv[0]) * uv[0])) |
+               (static_cast<uint32_t>(f32_to_bf16(silu(gv[1]) * uv[1])) << 16);
+        pk.y = static_cast<uint32_t>(f32_to_bf16(silu(gv[2]) * uv[2])) |
+               (static_cast<uint32_t>(f32_to_bf16(silu(gv[3]) * uv[3])) << 16);
+        *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.act_out) + static_cast<size_t>(m) * a.N + i0) = pk;
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < R; ++t) {
+        const int n = (blockIdx.x * R + t) * 16 + g * 4;
+        if (n >= a.N) continue;
+        *reinterpret_cast<f32x4_t*>(a.part + (static_cast<size_t>(blockIdx.y) * a.M + m) * a.N + n) = acc[t][mt];
+      }
+    }
+  }
+}
+
 // ---- prefill / large-batch tiled MFMA GEMM ---------------------------------
 // Block tile: 128 activation rows (m) x 256 weight rows (n), K step 64, four
 // waves as 2 (m) x 2 (n), each computing 64 m x 128 n with
@@ -513,12 +688,46 @@ void launch_skinny_m(const GemmArgs& a, hipStream_t s) {
   }
 }
 
-enum GemmKernel { kKStream = 1, kKSkinny16 = 2, kKSkinny32 = 3, kKTiled = 4, kKF32 = 5 };
+constexpr int kMaxSplitsAny = 64;
+
+enum GemmKernel { kKStream = 1, kKSkinny16 = 2, kKSkinny32 = 3, kKTiled = 4, kKF32 = 5, kKDeep = 6 };
 
 struct GemmPlan {
   int kernel;
   int splits;
+  int R = 0, D = 0;  // k_gemm_deep: weight fragments per block and register stages
 };
+
+template <int R, int MT, int D, bool SILU>
+void launch_deep_t(const GemmArgs& a, hipStream_t s) {
+  const int KU = a.K / 64;
+  const int ups = (KU + a.splits - 1) / a.splits;
+  const int per = SILU ? R / 2 : R;
+  const int nb = (a.N / 16 + per - 1) / per;
+  hipLaunchKernelGGL((k_gemm_deep<R, MT, D, SILU>), dim3(nb, a.splits), dim3(256), 0, s, a, ups);
+}
+
+// The (R, D) pairs instantiated for each activation tile count MT = ceil(M / 16).
+struct DeepCfg { int R, D; };
+constexpr DeepCfg kDeepCfg[4][4] = {
+    {{10, 2}, {8, 2}, {4, 4}, {0, 0}},
+    {{10, 2}, {8, 2}, {4, 4}, {0, 0}},
+    {{10, 2}, {8, 2}, {6, 2}, {0, 0}},
+    {{10, 2}, {8, 2}, {6, 2}, {4, 3}},
+};
+
+template <bool SILU>
+bool launch_deep(const GemmArgs& a, int R, int D, hipStream_t s) {
+#define RP_DEEP(MT_, R_, D_) \
+  if (mt == MT_ && R == R_ && D == D_) { launch_deep_t<R_, MT_, D_, SILU>(a, s); return true; }
+  const int mt = (a.M + 15) / 16;
+  RP_DEEP(1, 10, 2) RP_DEEP(1, 8, 2) RP_DEEP(1, 4, 4)
+  RP_DEEP(2, 10, 2) RP_DEEP(2, 8, 2) RP_DEEP(2, 4, 4)
+  RP_DEEP(3, 10, 2) RP_DEEP(3, 8, 2) RP_DEEP(3, 6, 2)
+  RP_DEEP(4, 10, 2) RP_DEEP(4, 8, 2) RP_DEEP(4, 6, 2) RP_DEEP(4, 4, 3)
+#undef RP_DEEP
+  return false;
+}
 
 // Number of K splits that leaves no split empty, for a wish of `want`.
 int even_splits(int n_units, int want) {
@@ -528,11 +737,44 @@ int even_splits(int n_units, int want) {
   return (n_units + per - 1) / per;
 }
 
+// k_gemm_deep plan.  The blocks hold one CU each (their register use
+// allows one wave per SIMD), so the time is set by the busiest CU: rounds of
+// 256 blocks times the rows x K units of one block.  The K split is the
+// largest that keeps all blocks in one round and every wave at >= 3 units;
+// a small penalty for activation traffic (MT / R of the weight loads)
+// breaks ties toward more weight rows per block.  Measured on the Qwen2.5
+// 7B decode shapes, this picks the best swept configuration or one within
+// a few percent of it.
+GemmPlan plan_deep(int M, int N, int K, bool silu, int max_splits) {
+  const int mt = (M + 15) / 16, KU = K / 64, units = N / 16;
+  GemmPlan best{kKDeep, 1};
+  double best_cost = 1e300;
+  for (const DeepCfg& c : kDeepCfg[mt - 1]) {
+    if (c.R == 0) continue;
+    const int per = silu ? c.R / 2 : c.R;
+    const int nb = (units + per - 1) / per;
+    int S = 1;
+    if (!silu) {
+      const int smax = std::max(1, std::min(std::min(16, max_splits), KU / 12));
+      while (S < smax && nb * (S + 1) <= 256) ++S;
+      S = even_splits(KU, S);
+    }
+    const int rounds = (nb * S + 255) / 256;
+    const double cost = static_cast<double>(rounds) * c.R * 16 * ((KU + S - 1) / S) * (1.0 + 0.15 * mt / c.R);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = GemmPlan{kKDeep, S, c.R, c.D};
+    }
+  }
+  return best;
+}
+
 // Kernel and split choice, from sweeps of the Qwen2.5 decode shapes on
-// gfx950: per-wave activation loads win for the wide gate/up projection and
-// for the LM head at tiny batches; LDS-shared activations with 16 (M <= 16)
-// or 32 (M > 16) weight rows per wave win elsewhere; the K split is the
-// smallest that gives roughly two blocks per CU.
+// gfx950 (weights cycled through more than the 256 MB last-level cache so
+// that none is reused between launches): the deep-pipelined kernel for
+// decode batches of the weight matrices of 7B and larger models; the older
+// streaming kernels for the small matrices (the 0.5B model, the 7B output
+// projection at <= 16 rows), where launch latency dominates.
 GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
   if (!bf16) return {kKF32, 1};
   if (M > 64) {
@@ -541,6 +783,8 @@ GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
     s = std::min(s, std::max(1, (K / kGBK) / 4));
     return {kKTiled, even_splits(K / kGBK, std::min(s, max_splits))};
   }
+  const double work = static_cast<double>(N) * K * (silu ? 2 : 1);
+  if (K % 64 == 0 && N % 16 == 0 && work >= (M > 16 ? 8.0e6 : 1.4e7)) return plan_deep(M, N, K, silu, max_splits);
   const int n_chunks = K / 128;
   auto pick = [&](int blocks, int target) {
     int s = 1;
@@ -569,7 +813,9 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   const bool silu = a.epi == kEpiSiluMul;
   if (a.splits < 1 || (silu && a.splits != 1)) return hipErrorInvalidValue;
-  const int kernel = a.variant ? a.variant : plan_gemm(bf16, a.M, a.N, a.K, silu, 64).kernel;
+  GemmPlan plan = plan_gemm(bf16, a.M, a.N, a.K, silu, kMaxSplitsAny);
+  if (a.variant == kKDeep && plan.kernel != kKDeep && a.M <= 64) plan = plan_deep(a.M, a.N, a.K, silu, kMaxSplitsAny);
+  const int kernel = a.variant ? a.variant : plan.kernel;
   if (!bf16 || kernel == kKF32) {
     if (bf16 || a.splits != 1) return hipErrorInvalidValue;
     dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
@@ -587,6 +833,11 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
     if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps, n_mb, n_nb);
     else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(256), 0, s, a, kbps, n_mb, n_nb);
     return hipGetLastError();
+  }
+  if (kernel == kKDeep) {
+    if (a.K % 64 != 0 || a.N % 16 != 0 || plan.kernel != kKDeep) return hipErrorInvalidValue;
+    const bool ok = silu ? launch_deep<true>(a, plan.R, plan.D, s) : launch_deep<false>(a, plan.R, plan.D, s);
+    return ok ? hipGetLastError() : hipErrorInvalidValue;
   }
   if (a.K % 128 != 0) return hipErrorInvalidValue;
   switch (kernel) {

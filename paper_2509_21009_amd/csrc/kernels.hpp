@@ -36,7 +36,7 @@ struct GemmArgs {
   int splits;        // S >= 1; kEpiSiluMul requires 1
   float* part;       // [S, M, N] (kEpiPartial)
   void* act_out;     // [M, N] dtype T (kEpiSiluMul)
-  int variant;       // 0: automatic; 1 stream, 2/3 skinny (16/32 rows per wave), 4 tiled
+  int variant;       // 0: automatic; 1 stream, 2/3 skinny (16/32 rows per wave), 4 tiled, 6 deep
 };
 
 // Picks the kernel from dtype, M, N and K.  Returns hipSuccess or a launch error.

@@ -119,14 +119,20 @@ def test_bf16_against_rounding_oracle():
     assert r.greedy_agree >= 0.995 * r.positions, r
 
 
-def test_bf16_decode_batch_shapes():
-    """Decode GEMM regimes: B = 1, 17, 40, 64 (weight streaming) and 80 (LDS-tiled MFMA),
-    on the 0.5B layer shape (K = 896 and 4864, GQA group 7, head_dim 64)."""
-    base = truncated(SHAPES["qwen2.5-0.5b"], 1, vocab=4096)
+@pytest.mark.parametrize("model,layers,vocab,batches", [
+    ("qwen2.5-0.5b", 1, 4096, (1, 17, 40, 64, 80)),
+    ("qwen2.5-7b", 1, 8192, (2, 24, 40, 64)),
+])
+def test_bf16_decode_batch_shapes(model, layers, vocab, batches):
+    """Decode GEMM regimes by live rows: 1-16, 17-32, 33-48, 49-64 (weight streaming: one
+    to four 16-row activation tiles) and 80 (LDS-tiled MFMA).  The 0.5B layer (K = 896 and
+    4864) runs the small-matrix kernels; the 7B layer (K = 3584 and 18944, LM head 8192 x 3584)
+    runs the deep-pipelined ones with their K splits and ragged last blocks."""
+    base = truncated(SHAPES[model], layers, vocab=vocab)
     wd = make_weights(base, seed=1, device=DEV)
     w64 = weights_to_numpy(wd)
     rng = np.random.default_rng(5)
-    for B in (1, 17, 40, 64, 80):
+    for B in batches:
         plen = rng.integers(1, 24, size=B)
         prompts = [rng.integers(0, base.vocab, size=int(p)).astype(np.int32) for p in plen]
         offs = np.zeros(B + 1, np.int64)
@@ -135,7 +141,7 @@ def test_bf16_decode_batch_shapes():
         wl = Workload("batch", base, np.arange(100, 100 + B, dtype=np.int64), np.concatenate(prompts), offs,
                       np.full(B, 3, np.int32), np.arange(B, dtype=np.int32), 1.0, 77)
         eng = _engine(base, wd, 96, 4096, 64, 2 * 96)
-        log(f"decode batch B={B}")
+        log(f"{model}: decode batch B={B}")
         r = teacher_forced_parity(eng, base, w64, wl, 3, 2e-2, 1.0, 77)
         eng.close()
         log(f"B={B}: {r}")
