@@ -77,7 +77,8 @@ ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l) {
   p.part_elems = std::max(static_cast<size_t>(l.max_prefill_tokens) * nmax,
                           static_cast<size_t>(kMaxGemmSplits) * l.max_seqs * nmax);
   const size_t T = l.max_prefill_tokens, S = l.max_seqs;
-  p.meta_ints = static_cast<int32_t>(std::max(7 * S + 1, 3 * T + 8 * S + 1));
+  // decode: 7 ints per row + 1, padded to 16 bytes, then 4 per split; prefill: 3 per token + 8 per row + 1
+  p.meta_ints = static_cast<int32_t>(std::max(7 * S + 4 + 4 * static_cast<size_t>(p.split_cap), 3 * T + 8 * S + 1));
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
   p.x = take(mmax * H * 4);
@@ -351,7 +352,7 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
       launch_timed(RP_K_ATTN, attn_bytes, attn_flops, [&] { return launch_attn_prefill(bf16_, aa, s); });
     } else {
       aa.B = M; aa.row_slot = m_slot_; aa.row_ctx = m_ctx_; aa.split_off = m_split_off_;
-      aa.total_splits = total_splits; aa.tokens_per_split = tps;
+      aa.total_splits = total_splits; aa.tokens_per_split = tps; aa.split_desc = m_split_desc_;
       aa.part_o = sp<float>(plan_.att_o); aa.part_ml = sp<float>(plan_.att_ml);
       launch_timed(RP_K_ATTN, attn_bytes, attn_flops, [&] { return launch_attn_decode(bf16_, aa, s); });
       if (bf16_) {
@@ -533,7 +534,27 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     for (int i = 0; i < B; ++i)
       if (forced[i] < 0 || forced[i] >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "forced token out of range");
   }
-  const size_t ints = 7 * static_cast<size_t>(B) + 1;
+  // Per-row context first: the split plan sizes the metadata.
+  std::vector<int32_t>& ctx_h = ctx_scratch_;
+  ctx_h.resize(B);
+  int64_t total_pages = 0;
+  sum_ctx_ = 0;
+  for (int i = 0; i < B; ++i) {
+    const Seq& q = slots_[rows[i]];
+    ctx_h[i] = q.prompt_len + q.n_gen;
+    total_pages += PagePool::pages_for(ctx_h[i], kPageTokens);
+    sum_ctx_ += ctx_h[i];
+  }
+  int tps = 0, total_splits = 0;
+  if (bf16_) {
+    const int64_t target = decode_split_target(cfg_);
+    const int64_t pps = std::max<int64_t>(1, (total_pages + target - 1) / target);
+    tps = static_cast<int>(pps * kPageTokens);
+    for (int i = 0; i < B; ++i) total_splits += (ctx_h[i] + tps - 1) / tps;
+    if (total_splits > plan_.split_cap) throw RpError(RP_ERR_CAPACITY, "decode split capacity exceeded");
+  }
+  const size_t desc_at = (7 * static_cast<size_t>(B) + 1 + 3) & ~static_cast<size_t>(3);
+  const size_t ints = desc_at + 4 * static_cast<size_t>(total_splits);
   int32_t* m = stage_meta(ints);
   int32_t* in_tok = m;
   int32_t* slot = in_tok + B;
@@ -542,8 +563,8 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
   int32_t* split_off = ctx + B;
   int32_t* gen_pos = split_off + B + 1;
   int32_t* gen_hist = gen_pos + B;
-  int64_t total_pages = 0;
-  sum_ctx_ = 0;
+  int32_t* desc = m + desc_at;
+  int32_t sx = 0;
   for (int i = 0; i < B; ++i) {
     const Seq& q = slots_[rows[i]];
     in_tok[i] = forced ? forced[i] : -1;
@@ -552,27 +573,24 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     ctx[i] = pos[i] + 1;
     gen_pos[i] = pos[i] + 1;
     gen_hist[i] = q.n_gen;
-    total_pages += PagePool::pages_for(ctx[i], kPageTokens);
-    sum_ctx_ += ctx[i];
-  }
-  int tps = 0, total_splits = 0;
-  if (bf16_) {
-    const int64_t target = decode_split_target(cfg_);
-    const int64_t pps = std::max<int64_t>(1, (total_pages + target - 1) / target);
-    tps = static_cast<int>(pps * kPageTokens);
-    for (int i = 0; i < B; ++i) {
-      split_off[i] = total_splits;
-      total_splits += (ctx[i] + tps - 1) / tps;
+    split_off[i] = sx;
+    if (bf16_) {
+      // one descriptor per split: row (+ 2^30 when it is the row's only split), key range, slot
+      const int n = (ctx[i] + tps - 1) / tps;
+      for (int j = 0; j < n; ++j, ++sx) {
+        desc[4 * sx + 0] = i | (n == 1 ? (1 << 30) : 0);
+        desc[4 * sx + 1] = j * tps;
+        desc[4 * sx + 2] = std::min(j * tps + tps, ctx[i]);
+        desc[4 * sx + 3] = rows[i];
+      }
     }
-    if (total_splits > plan_.split_cap) throw RpError(RP_ERR_CAPACITY, "decode split capacity exceeded");
-  } else {
-    for (int i = 0; i < B; ++i) split_off[i] = 0;
   }
   split_off[B] = total_splits;
   upload_meta(m, ints);
   const int32_t* d = d_meta_;
   m_in_tok_ = d; m_slot_ = d + B; m_pos_ = d + 2 * B; m_ctx_ = d + 3 * B; m_split_off_ = d + 4 * B;
   m_gen_pos_ = d + 5 * B + 1; m_gen_hist_ = d + 6 * B + 1; m_gen_slot_ = m_slot_;
+  m_split_desc_ = d + desc_at;
   forward(B, false, 0, 0, total_splits, tps);
   if (logits_out) {
     HIP_TRY(hipMemcpyAsync(logits_out, scratch_ + plan_.logits, static_cast<size_t>(B) * cfg_.vocab * 4,

@@ -128,7 +128,8 @@ class Engine {
                 *m_ctx_ = nullptr, *m_split_off_ = nullptr, *m_seq_slot_ = nullptr,
                 *m_seq_row0_ = nullptr, *m_seq_pos0_ = nullptr, *m_seq_ntok_ = nullptr,
                 *m_item_off_ = nullptr, *m_last_row_ = nullptr, *m_gen_pos_ = nullptr,
-                *m_gen_hist_ = nullptr, *m_gen_slot_ = nullptr;
+                *m_gen_hist_ = nullptr, *m_gen_slot_ = nullptr, *m_split_desc_ = nullptr;
+  std::vector<int32_t> ctx_scratch_;  // decode_step: per-row context lengths
   std::vector<hipEvent_t> events_;
 
   // per-kernel-class profiling (rp_profile_*)

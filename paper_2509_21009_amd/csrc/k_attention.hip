@@ -2,17 +2,20 @@
 //
 // One 64-lane wave owns a work item: up to 16 query rows that share one KV
 // head (the G query heads of a token, or G heads x floor(16/G) tokens in
-// prefill) and a range of KV tokens.  Per 64-token page it computes
-// S^T = K Q^T as four 16x16 MFMA tiles, runs an online softmax in the log2
-// domain, and accumulates O^T = V^T P^T with MFMA.  V pages are stored
-// transposed ([hd][64 tokens]) so both MFMA operands are read as contiguous
-// 16-byte runs straight from HBM; the page's tokens are assigned to MFMA
-// rows so that each lane's softmax outputs are exactly the P^T operand it
-// must supply, with no data exchange between lanes.
+// prefill) and a range of KV tokens.  Per 32-token half page it computes
+// S^T = K Q^T as two 16x16 MFMA tiles, runs an online softmax in the log2
+// domain, and accumulates O^T = V^T P^T with MFMA.  A V page is stored as
+// two 32-token halves, each transposed ([hd][32 tokens]), so that one
+// half's V operands are a contiguous 8 KB run and both MFMA operands are read
+// as 16-byte pieces straight from HBM; the tokens are assigned to MFMA rows
+// so that each lane's softmax outputs are exactly the P^T operand it must
+// supply, with no data exchange between lanes.
 //
-// Decode splits each sequence's context into chunks (one work item each) so
-// that small batches with long contexts still spread over all CUs; a merge
-// kernel combines the chunk maxima, sums and partial outputs.
+// Decode splits each sequence's context into chunks (one work item each, with
+// a host-built descriptor) so that small batches with long contexts still
+// spread over all CUs; the half pages of an item stream through a ring of
+// register stages.  A merge kernel combines the chunk maxima, sums and
+// partial outputs.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -56,7 +59,7 @@ __device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, 
 #pragma unroll
   for (int blk = 0; blk < HD / 16; ++blk)
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp) vf[blk][pp] = load_bf16x8(vb + (blk * 16 + c) * kPageTokens + 32 * pp + 8 * g);
+    for (int pp = 0; pp < 2; ++pp) vf[blk][pp] = load_bf16x8(vb + pp * HD * 32 + (blk * 16 + c) * 32 + 8 * g);
 
   float sv[16];
   float pmax = -INFINITY;
@@ -105,20 +108,13 @@ __device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, 
 
 template <int HD>
 __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
-  constexpr int KS = HD / 32, HQ = HD / 4;
+  constexpr int KS = HD / 32, HQ = HD / 4, NB = HD / 16, D = 2;
   const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
   const int x = blockIdx.x, kh = blockIdx.y;
-  int lo = 0, hi = a.B;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (a.split_off[mid] <= x) lo = mid; else hi = mid;
-  }
-  const int b = lo;
-  const int s = x - a.split_off[b];
-  const int ctx = a.row_ctx[b];
-  const int t0 = s * a.tokens_per_split;
-  const int t1 = min(t0 + a.tokens_per_split, ctx);
-  const int slot = a.row_slot[b];
+  const int4 dsc = reinterpret_cast<const int4*>(a.split_desc)[x];
+  const int b = dsc.x & 0x3fffffff;
+  const bool single = (dsc.x >> 30) & 1;
+  const int t0 = dsc.y, t1 = dsc.z, slot = dsc.w;
   const int G = a.n_q / a.n_kv;
 
   bf16x8_t qf[KS];
@@ -130,32 +126,142 @@ __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
   }
-  f32x4_t o[HD / 16];
-#pragma unroll
-  for (int blk = 0; blk < HD / 16; ++blk) o[blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  SoftmaxState st{-INFINITY, 0.f};
+  // Lane i holds the page of the item's i-th page (the first 64 pages; later
+  // ones, for items longer than 4096 tokens, are read from the table).
+  const int* pt = a.page_table + static_cast<size_t>(slot) * a.pt_stride;
+  const int p0 = t0 / kPageTokens;
+  const int npg = (t1 + kPageTokens - 1) / kPageTokens - p0;
+  const int ptv = lane < npg ? pt[p0 + lane] : 0;
+  const int u0 = t0 >> 5;
+  const int nu = ((t1 + 31) >> 5) - u0;  // half pages of the item
   const bf16_t* kpool = static_cast<const bf16_t*>(a.k_pool);
   const bf16_t* vpool = static_cast<const bf16_t*>(a.v_pool);
   const float scale_log2 = a.scale * kLog2e;
-  const int* pt = a.page_table + static_cast<size_t>(slot) * a.pt_stride;
-  for (int p = t0 / kPageTokens; p * kPageTokens < t1; ++p) {
-    const size_t pb = (static_cast<size_t>(pt[p]) * a.n_kv + kh) * kPageTokens * HD;
-    attend_page<HD>(kpool + pb, vpool + pb, p * kPageTokens, qf, 0x7fffffff, t0, t1, scale_log2, st, o);
+
+  bf16x8_t kf[D][2][KS], vf[D][NB];
+  auto load = [&](int sl, int i) {
+    const int u = u0 + min(i, nu - 1);  // prologue stages past the item re-read its last half page
+    const int pi = (u >> 1) - p0;
+    const int pg = pi < 64 ? __builtin_amdgcn_readlane(ptv, pi) : pt[p0 + pi];
+    const int h = u & 1;
+    const size_t pb = (static_cast<size_t>(pg) * a.n_kv + kh) * kPageTokens * HD;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      // MFMA row c of S^T tile (2h + tt) of the page is token 32h + 8(c >> 2) + 4tt + (c & 3)
+      const bf16_t* krow = kpool + pb + (32 * h + 8 * (c >> 2) + 4 * tt + (c & 3)) * HD + g * HQ;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kf[sl][tt][ks] = load_bf16x8(krow + ks * 8);
+    }
+    const bf16_t* vh = vpool + pb + h * HD * 32;
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) vf[sl][blk] = load_bf16x8(vh + (blk * 16 + c) * 32 + 8 * g);
+  };
+
+  f32x4_t o[NB];
+#pragma unroll
+  for (int blk = 0; blk < NB; ++blk) o[blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  auto compute = [&](int sl, int i) {
+    const int u = u0 + i;
+    f32x4_t sacc[2];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      sacc[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) sacc[tt] = mfma16x16x32(kf[sl][tt][ks], qf[ks], sacc[tt]);
+    }
+    float sv[8];
+    float pmax = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int tok = 32 * u + 8 * g + 4 * tt + e;
+        float v = sacc[tt][e] * scale_log2;
+        if (tok < t0 || tok >= t1) v = -INFINITY;
+        sv[tt * 4 + e] = v;
+        pmax = fmaxf(pmax, v);
+      }
+    pmax = fmaxf(pmax, __shfl_xor(pmax, 16, 64));
+    pmax = fmaxf(pmax, __shfl_xor(pmax, 32, 64));
+    const float m_new = fmaxf(m_run, pmax);
+    const float shift = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = exp2f(m_run - shift);
+    float psum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      sv[k] = exp2f(sv[k] - shift);
+      psum += sv[k];
+    }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    uint4 w;
+    w.x = static_cast<uint32_t>(f32_to_bf16(sv[0])) | (static_cast<uint32_t>(f32_to_bf16(sv[1])) << 16);
+    w.y = static_cast<uint32_t>(f32_to_bf16(sv[2])) | (static_cast<uint32_t>(f32_to_bf16(sv[3])) << 16);
+    w.z = static_cast<uint32_t>(f32_to_bf16(sv[4])) | (static_cast<uint32_t>(f32_to_bf16(sv[5])) << 16);
+    w.w = static_cast<uint32_t>(f32_to_bf16(sv[6])) | (static_cast<uint32_t>(f32_to_bf16(sv[7])) << 16);
+    const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, w);
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) o[blk] = mfma16x16x32(vf[sl][blk], pf, o[blk] * alpha);
+  };
+
+  if (nu > 0) {
+    // Unconditional prologue and scheduling barriers: every path into the
+    // main loop has the same loads in flight, so its wait counts are exact.
+#pragma unroll
+    for (int sl = 0; sl < D; ++sl) {
+      load(sl, sl);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    int i = 0;
+    for (; i + 2 * D <= nu; i += D) {
+#pragma unroll
+      for (int sl = 0; sl < D; ++sl) {
+        compute(sl, i + sl);
+        __builtin_amdgcn_sched_barrier(0);
+        load(sl, i + sl + D);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 2 * D; ++j) {
+      if (i + j < nu) {
+        compute(j % D, i + j);
+        __builtin_amdgcn_sched_barrier(0);
+        if (i + j + D < nu) load(j % D, i + j + D);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+
+  if (c >= G) return;
+  if (single) {  // the row's only split: normalise and write the output directly
+    const float inv = 1.f / l_run;
+    bf16_t* orow = static_cast<bf16_t*>(a.out) + (static_cast<size_t>(b) * a.n_q + kh * G + c) * HD;
+#pragma unroll
+    for (int blk = 0; blk < NB; ++blk) {
+      uint2 pk;
+      pk.x = static_cast<uint32_t>(f32_to_bf16(o[blk][0] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[blk][1] * inv)) << 16);
+      pk.y = static_cast<uint32_t>(f32_to_bf16(o[blk][2] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[blk][3] * inv)) << 16);
+      *reinterpret_cast<uint2*>(orow + blk * 16 + 4 * g) = pk;
+    }
+    return;
   }
   const size_t item = static_cast<size_t>(x) * a.n_kv + kh;
-  if (c < G) {
-    float* po = a.part_o + (item * 16 + c) * HD;
+  float* po = a.part_o + (item * 16 + c) * HD;
 #pragma unroll
-    for (int blk = 0; blk < HD / 16; ++blk)
-      *reinterpret_cast<float4*>(po + blk * 16 + 4 * g) = make_float4(o[blk][0], o[blk][1], o[blk][2], o[blk][3]);
-    if (g == 0) {
-      a.part_ml[item * 32 + c] = st.m;
-      a.part_ml[item * 32 + 16 + c] = st.l;
-    }
+  for (int blk = 0; blk < NB; ++blk)
+    *reinterpret_cast<float4*>(po + blk * 16 + 4 * g) = make_float4(o[blk][0], o[blk][1], o[blk][2], o[blk][3]);
+  if (g == 0) {
+    a.part_ml[item * 32 + c] = m_run;
+    a.part_ml[item * 32 + 16 + c] = l_run;
   }
 }
 
-// One block per (row, query head) with HD x 8 threads: the splits' maxima
+// One block per (row, query head) with HD x 8 threads (rows with more than
+// one split): the splits' maxima
 // and sums are staged in LDS, each of 8 thread groups accumulates every 8th
 // split for all HD output elements, and the groups are summed in LDS.  Long
 // contexts at small batch have hundreds of splits, which a single serial
@@ -174,6 +280,7 @@ __global__ __launch_bounds__(HD * kMergeGroups) void k_attn_merge(AttnArgs a) {
   const int G = a.n_q / a.n_kv;
   const int kh = h / G, c = h % G;
   const int s0 = a.split_off[b], n = a.split_off[b + 1] - s0;
+  if (n <= 1) return;  // single-split rows were written by the decode kernel
   const int nc = min(n, kMergeCache);
   auto m_of = [&](int t) { return a.part_ml[(static_cast<size_t>(s0 + t) * a.n_kv + kh) * 32 + c]; };
   auto l_of = [&](int t) { return a.part_ml[(static_cast<size_t>(s0 + t) * a.n_kv + kh) * 32 + 16 + c]; };
@@ -289,8 +396,9 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
     l = l * alpha + p;
     m = m_new;
     const float* v = vpool + pb;
-    if (lane < HD) acc[0] = acc[0] * alpha + p * v[static_cast<size_t>(lane) * kPageTokens + off];
-    if (lane + 64 < HD) acc[1] = acc[1] * alpha + p * v[static_cast<size_t>(lane + 64) * kPageTokens + off];
+    const float* vh = v + (off >> 5) * HD * 32 + (off & 31);
+    if (lane < HD) acc[0] = acc[0] * alpha + p * vh[static_cast<size_t>(lane) * 32];
+    if (lane + 64 < HD) acc[1] = acc[1] * alpha + p * vh[static_cast<size_t>(lane + 64) * 32];
   }
   float* out = static_cast<float*>(a.out) + (static_cast<size_t>(i) * a.n_q + h) * HD;
   if (lane < HD) out[lane] = acc[0] / l;
@@ -313,7 +421,7 @@ hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   if (a.B <= 0 || a.total_splits <= 0) return hipSuccess;
-  if (a.n_q / a.n_kv > 16 || a.tokens_per_split % kPageTokens != 0) return hipErrorInvalidValue;
+  if (a.n_q / a.n_kv > 16 || a.tokens_per_split % kPageTokens != 0 || !a.split_desc) return hipErrorInvalidValue;
   dim3 grid(a.total_splits, a.n_kv);
   if (a.hd == 128) hipLaunchKernelGGL(k_attn_decode_bf16<128>, grid, dim3(64), 0, s, a);
   else if (a.hd == 64) hipLaunchKernelGGL(k_attn_decode_bf16<64>, grid, dim3(64), 0, s, a);

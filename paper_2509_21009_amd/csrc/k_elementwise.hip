@@ -178,7 +178,8 @@ __global__ __launch_bounds__(256) void k_rope_append(RopeArgs a) {
 #pragma unroll
     for (int s = 0; s < S; ++s) v += prow[s * plane + n];
     v += Elem<T>::load(static_cast<const T*>(a.bv), e);
-    const size_t idx = ((static_cast<size_t>(page) * a.n_kv + kh) * hd + d) * kPageTokens + off;
+    // V page: two 32-token halves, each [hd][32 tokens]
+    const size_t idx = (static_cast<size_t>(page) * a.n_kv + kh) * hd * kPageTokens + (off >> 5) * hd * 32 + d * 32 + (off & 31);
     Elem<T>::store(static_cast<T*>(a.v_pool), idx, v);
   }
 }

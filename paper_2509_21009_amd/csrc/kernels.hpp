@@ -84,6 +84,7 @@ struct AttnArgs {
   // decode (one query token per sequence, split over the context):
   int B; const int32_t* row_slot; const int32_t* row_ctx; const int32_t* split_off;
   int total_splits; int tokens_per_split;
+  const int32_t* split_desc;      // [total_splits, 4]: row (+ 2^30 if its only split), first key, end key, slot
   float* part_o; float* part_ml;  // [total_splits * n_kv, 16, hd], [.., 2, 16]
   // prefill (causal over packed prompt chunks):
   int n_seq; const int32_t* seq_slot; const int32_t* seq_row0; const int32_t* seq_pos0;

@@ -148,6 +148,29 @@ def test_bf16_decode_batch_shapes(model, layers, vocab, batches):
         assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, (B, r)
 
 
+def test_long_context_many_splits():
+    """One 4150-token row beside two short ones: its decode context spans 65 pages, so the
+    split-context attention runs 65 work items for that row and the merge walks two chunks
+    of 64 splits; the short rows are single-split items written without a merge."""
+    s = truncated(SHAPES["qwen2.5-0.5b"], 1, vocab=2048)
+    s = dataclasses.replace(s, tied=False)
+    wd = make_weights(s, seed=6, device=DEV)
+    w64 = weights_to_numpy(wd)
+    rng = np.random.default_rng(21)
+    plen = [4150, 17, 40]
+    prompts = [rng.integers(0, s.vocab, size=p).astype(np.int32) for p in plen]
+    offs = np.zeros(4, np.int64)
+    offs[1:] = np.cumsum(plen)
+    from workloads.gen import Workload
+    wl = Workload("long", s, np.array([7, 8, 9], np.int64), np.concatenate(prompts), offs,
+                  np.full(3, 4, np.int32), np.arange(3, dtype=np.int32), 1.0, 5)
+    eng = _engine(s, wd, 4, 4200, 4224, 3 * 67)
+    r = teacher_forced_parity(eng, s, w64, wl, 4, 2e-2, 1.0, 5)
+    eng.close()
+    log(f"long context: {r}")
+    assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, r
+
+
 def test_page_boundaries_chunked_prefill_and_short_sequences():
     """Prompts of 1, 63, 64, 65 and 130 tokens, max_new 1 and 70 (decode crosses pages),
     prefill split into chunks of at most 140 tokens."""
