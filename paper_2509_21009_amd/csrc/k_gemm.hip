@@ -448,97 +448,114 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
 }
 
 // ---- prefill / large-batch tiled MFMA GEMM ---------------------------------
-// Block tile: 128 activation rows (m) x 256 weight rows (n), K step 64, four
-// waves as 2 (m) x 2 (n), each computing 64 m x 128 n with
-// v_mfma_f32_32x32x16_bf16 (2 x 4 tiles, 128 fp32 accumulators per lane).
-// Activations are the MFMA row operand and weights the column operand, so
-// the 32 lanes of one accumulator register hold 32 consecutive n: coalesced
-// stores.  Two padded LDS stages; the next K step is prefetched into
-// registers while the current one is multiplied; one barrier per K step.
+// Block tile: 256 activation rows (m) x 256 weight rows (n), K step 64, eight
+// waves as 2 (m) x 4 (n), each computing 128 m x 64 n with
+// v_mfma_f32_32x32x16_bf16 (4 x 2 tiles, 128 fp32 accumulators per lane; two
+// waves per SIMD).  Activations are the MFMA row operand and weights the
+// column operand, so the 32 lanes of one accumulator register hold 32
+// consecutive n: coalesced stores.  Tiles move HBM -> registers -> padded
+// LDS (two stages); the next K step is loaded into registers while the
+// current one is multiplied, one barrier per K step, and each wave
+// double-buffers its LDS fragments across the four 16-wide MFMA k-steps.
+// Global loads go through buffer resources: a wave's 8-row slab of a weight
+// tile lies in one weight segment, and rows past M or N read as zeros.
 // Tiles are ordered so that the blocks an XCD runs back to back (ids equal
 // mod 8) walk the m tiles of one weight panel, which then stays in that
 // XCD's L2.
-constexpr int kGBM = 128, kGBN = 256, kGBK = 64, kGLD = kGBK + 8;
+constexpr int kGBM = 256, kGBN = 256, kGBK = 64, kGLD = kGBK + 8;
 
 template <bool SILU>
-__global__ __launch_bounds__(256) void k_gemm_tiled(GemmArgs a, int kblocks_per_split, int n_mb, int n_nb) {
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][kGBM * kGLD];
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[2][kGBN * kGLD];
+__global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_split, int n_mb, int n_nb) {
+  // one LDS array: stage st of the activation tile at st * kGBM * kGLD, of the weight tile
+  // after both activation stages (two separate arrays cost registers for their bases)
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (kGBM + kGBN) * kGLD];
+  bf16_t* const As = smem;
+  bf16_t* const Ws = smem + 2 * kGBM * kGLD;
   const int n_tiles = n_mb * n_nb;
   const int per_xcd = (n_tiles + 7) / 8;
   const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if (t >= n_tiles) return;  // block-uniform: padding of the XCD-ordered grid
   const int nb = t / n_mb, mb = t % n_mb;
   const int split = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
   const int l32 = lane & 31, lh = lane >> 5;
   const int K = a.K;
 
-  // global -> LDS assignment: A 128 rows x 8 pieces (4 per thread), W 256 rows x 8 pieces (8 per thread)
-  const bf16_t* asrc[4];
-  const bf16_t* wsrc[8];
+  // global -> LDS staging: thread rows (tid >> 3) + 64 i, 16-byte column piece (tid & 7)
+  const int trow = tid >> 3, tcol = (tid & 7) * 8;
+  const __amdgpu_buffer_rsrc_t ars = buffer_rsrc(a.A, static_cast<uint32_t>(a.M) * static_cast<uint32_t>(a.lda) * 2u);
+  int aoff[4], woff[4];
+  __amdgpu_buffer_rsrc_t wrs[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int q = tid + 256 * i, row = q >> 3, col = (q & 7) * 8;
-    int m = mb * kGBM + row;
-    if (m >= a.M) m = a.M - 1;
-    asrc[i] = static_cast<const bf16_t*>(a.A) + static_cast<size_t>(m) * a.lda + col;
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int q = tid + 256 * i, row = q >> 3, col = (q & 7) * 8;
-    if (SILU) {
-      const int grp = row >> 5;  // 32-row groups alternate gate / up over the same indices
-      const int idx = nb * 128 + (grp >> 1) * 32 + (row & 31);
-      wsrc[i] = static_cast<const bf16_t*>(a.W.ptr[grp & 1]) + static_cast<size_t>(idx) * K + col;
+    aoff[i] = ((mb * kGBM + trow + 64 * i) * static_cast<int>(a.lda) + tcol) * 2;
+    const int r0 = wave * 8 + 64 * i;  // the wave's 8-row slab of the weight tile
+    const bf16_t* wb;
+    int rel0, rows_valid;
+    if (SILU) {  // 32-row groups alternate gate / up over the same output indices
+      const int grp = r0 >> 5;
+      wb = static_cast<const bf16_t*>(a.W.ptr[grp & 1]);
+      rel0 = nb * 128 + (grp >> 1) * 32 + (r0 & 31);
+      rows_valid = a.N;
     } else {
-      int n = nb * kGBN + row;
-      if (n >= a.N) n = a.N - 1;
-      wsrc[i] = seg_row<bf16_t>(a.W, n, K) + col;
+      const int n0 = nb * kGBN + r0;
+      int b = 0, sg = 0;
+      while (sg < a.W.n_seg - 1 && n0 >= b + a.W.rows[sg]) b += a.W.rows[sg++];
+      wb = static_cast<const bf16_t*>(a.W.ptr[sg]);
+      rel0 = n0 - b;
+      rows_valid = n0 < a.N ? a.W.rows[sg] : 0;
     }
+    wrs[i] = buffer_rsrc(wb, static_cast<uint32_t>(rows_valid) * static_cast<uint32_t>(K) * 2u);
+    woff[i] = ((rel0 + (trow & 7)) * K + tcol) * 2;
   }
-  f32x16_t acc[2][4];
+  f32x16_t acc[4][2];
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+  for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+    for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[mt][nt][e] = 0.f;
 
   const int kb0 = split * kblocks_per_split;
   const int kb1 = min(kb0 + kblocks_per_split, K / kGBK);
-  uint4 ra[4], rw[8];
+  bf16x8_t ra[4], rw[4];
   auto load = [&](int kb) {
+    const int ko = kb * kGBK * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ra[i] = *reinterpret_cast<const uint4*>(asrc[i] + kb * kGBK);
+    for (int i = 0; i < 4; ++i) ra[i] = load_bf16x8(ars, aoff[i] + ko);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) rw[i] = *reinterpret_cast<const uint4*>(wsrc[i] + kb * kGBK);
+    for (int i = 0; i < 4; ++i) rw[i] = load_bf16x8(wrs[i], woff[i] + ko);
   };
   auto store = [&](int st) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int q = tid + 256 * i;
-      *reinterpret_cast<uint4*>(&As[st][(q >> 3) * kGLD + (q & 7) * 8]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int q = tid + 256 * i;
-      *reinterpret_cast<uint4*>(&Ws[st][(q >> 3) * kGLD + (q & 7) * 8]) = rw[i];
+      const int row = trow + 64 * i;
+      *reinterpret_cast<bf16x8_t*>(&As[st * kGBM * kGLD + row * kGLD + tcol]) = ra[i];
+      *reinterpret_cast<bf16x8_t*>(&Ws[st * kGBN * kGLD + row * kGLD + tcol]) = rw[i];
     }
   };
   auto compute = [&](int st) {
+    const bf16_t* as = As + st * kGBM * kGLD + (wm * 128 + l32) * kGLD + 8 * lh;
+    const bf16_t* ws = Ws + st * kGBN * kGLD + (wn * 64 + l32) * kGLD + 8 * lh;
+    bf16x8_t af[2][4], bw[2][2];
+    auto rd = [&](int buf, int kk) {
 #pragma unroll
-    for (int kk = 0; kk < kGBK; kk += 16) {
-      bf16x8_t af[2], bw[4];
+      for (int mt = 0; mt < 4; ++mt) af[buf][mt] = load_bf16x8(as + mt * 32 * kGLD + kk);
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) af[mt] = load_bf16x8(&As[st][(wm * 64 + mt * 32 + l32) * kGLD + kk + 8 * lh]);
+      for (int nt = 0; nt < 2; ++nt) bw[buf][nt] = load_bf16x8(ws + nt * 32 * kGLD + kk);
+    };
+    rd(0, 0);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) bw[nt] = load_bf16x8(&Ws[st][(wn * 128 + nt * 32 + l32) * kGLD + kk + 8 * lh]);
+    for (int ki = 0; ki < kGBK / 16; ++ki) {
+      if (ki + 1 < kGBK / 16) rd((ki + 1) & 1, (ki + 1) * 16);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma32x32x16(af[mt], bw[nt], acc[mt][nt]);
+        for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma32x32x16(af[ki & 1][mt], bw[ki & 1][nt], acc[mt][nt]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   if (kb0 < kb1) {
@@ -559,25 +576,22 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(GemmArgs a, int kblocks_per_
     __syncthreads();
   }
 
-  // acc[mt][nt] register e: m = wm*64 + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*128 + nt*32 + l32
+  // acc[mt][nt] register e: m = wm*128 + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*64 + nt*32 + l32
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+  for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const int m = mb * kGBM + wm * 64 + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+      const int m = mb * kGBM + wm * 128 + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
       if (m >= a.M) continue;
       if (SILU) {
-        bf16_t* out = static_cast<bf16_t*>(a.act_out) + static_cast<size_t>(m) * a.N;
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const int idx = nb * 128 + (wn * 2 + p) * 32 + l32;
-          out[idx] = f32_to_bf16(silu(acc[mt][2 * p][e]) * acc[mt][2 * p + 1][e]);
-        }
+        const int idx = nb * 128 + wn * 32 + l32;
+        static_cast<bf16_t*>(a.act_out)[static_cast<size_t>(m) * a.N + idx] =
+            f32_to_bf16(silu(acc[mt][0][e]) * acc[mt][1][e]);
       } else {
         float* out = a.part + (static_cast<size_t>(split) * a.M + m) * a.N;
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          const int n = nb * kGBN + wn * 128 + nt * 32 + l32;
+        for (int nt = 0; nt < 2; ++nt) {
+          const int n = nb * kGBN + wn * 64 + nt * 32 + l32;
           if (n < a.N) out[n] = acc[mt][nt][e];
         }
       }
@@ -779,7 +793,8 @@ GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
   if (!bf16) return {kKF32, 1};
   if (M > 64) {
     const int blocks = (silu ? N / 128 : (N + kGBN - 1) / kGBN) * ((M + kGBM - 1) / kGBM);
-    int s = silu ? 1 : (256 + blocks - 1) / blocks;
+    // one block per CU: the K split that keeps all blocks in one round of 256
+    int s = silu ? 1 : std::max(1, 256 / blocks);
     s = std::min(s, std::max(1, (K / kGBK) / 4));
     return {kKTiled, even_splits(K / kGBK, std::min(s, max_splits))};
   }
@@ -824,14 +839,20 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   if (kernel == kKTiled || a.M > 64) {
-    if (a.K % kGBK != 0 || (silu && a.N % 128 != 0) || (!silu && a.N % 32 != 0)) return hipErrorInvalidValue;
+    if (a.K % kGBK != 0 || (silu && a.N % 128 != 0) || (!silu && a.N % 8 != 0)) return hipErrorInvalidValue;
+    // 32-bit buffer offsets; every weight segment but the last a whole number of 8-row slabs
+    if (static_cast<int64_t>(a.M + kGBM) * a.lda * 2 >= (int64_t{1} << 31)) return hipErrorInvalidValue;
+    for (int sg = 0; sg < a.W.n_seg; ++sg) {
+      if (static_cast<int64_t>(a.W.rows[sg]) * a.K * 2 >= (int64_t{1} << 31)) return hipErrorInvalidValue;
+      if (!silu && sg < a.W.n_seg - 1 && a.W.rows[sg] % 8 != 0) return hipErrorInvalidValue;
+    }
     const int kbps = (a.K / kGBK + a.splits - 1) / a.splits;
     const int n_nb = silu ? a.N / 128 : (a.N + kGBN - 1) / kGBN;
     const int n_mb = (a.M + kGBM - 1) / kGBM;
     const int per_xcd = (n_mb * n_nb + 7) / 8;
     dim3 grid(8 * per_xcd, a.splits);
-    if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(256), 0, s, a, kbps, n_mb, n_nb);
-    else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(256), 0, s, a, kbps, n_mb, n_nb);
+    if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
+    else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
     return hipGetLastError();
   }
   if (kernel == kKDeep) {
