@@ -17,6 +17,7 @@ a single GPU.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -112,6 +113,23 @@ def cpu_baseline(weights, shape, wl):
             "extrapolated": True}
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of the roofline kernel from the calibrated FETCH_SIZE / WRITE_SIZE
+    counter runs recorded in profiles/, or None when there is no record for this kernel and
+    workload or the kernel's source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "gate_up_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError, KeyError):
+        return None
+    if rec.get("kernel") != kernel or rec.get("workload") != workload or rec.get("source_sha256") != digest:
+        return None
+    return int(rec["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,7 +212,8 @@ def main():
         bytes_per = p["bytes"] / p["launches"]
         achieved = bytes_per / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": args.kernel,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.kernel, args.workload),
+                "kernel": args.kernel,
                 "phase": "decode", "launches": p["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
                 "algorithmic_bytes_per_launch": bytes_per}
     out = {

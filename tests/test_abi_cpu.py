@@ -147,3 +147,14 @@ def test_workload_shapes_follow_the_configs():
     assert m.n == 576 and set(m.round_id.tolist()) == {0, 1} and len(set(m.seq_ids.tolist())) == 576
     c2 = make_workload("0.5b")
     assert c2.n == 256 and len(set(c2.prompt_group.tolist())) == 32
+
+
+def test_bench_reports_counter_traffic_only_for_the_measured_kernel():
+    """roofline.traffic comes from the calibrated counter record in profiles/ and is dropped
+    when the workload differs or the kernel source no longer matches the recorded hash."""
+    import json
+    import bench
+    rec = json.load(open(os.path.join(ROOT, "profiles", "gate_up_traffic.json")))
+    assert bench.measured_traffic("gemm_gate_up", "7b-long") == rec["traffic_bytes_per_launch"]
+    assert bench.measured_traffic("gemm_gate_up", "7b-short") is None
+    assert bench.measured_traffic("gemm_down", "7b-long") is None
