@@ -546,16 +546,27 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) bw[buf][nt] = load_bf16x8(ws + nt * 32 * kGLD + kk);
     };
+    // The next k-step's fragment reads are interleaved one-for-one with this
+    // k-step's MFMAs, at raised wave priority, so that the SIMD's other wave
+    // (in the same phase) finds MFMA issue slots between them.
     rd(0, 0);
 #pragma unroll
     for (int ki = 0; ki < kGBK / 16; ++ki) {
+      __builtin_amdgcn_s_setprio(1);
       if (ki + 1 < kGBK / 16) rd((ki + 1) & 1, (ki + 1) * 16);
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma32x32x16(af[ki & 1][mt], bw[ki & 1][nt], acc[mt][nt]);
-      __builtin_amdgcn_sched_barrier(0);
+      if (ki + 1 < kGBK / 16) {
+#pragma unroll
+        for (int q = 0; q < 6; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      }
+      __builtin_amdgcn_s_setprio(0);
     }
   };
   if (kb0 < kb1) {
