@@ -113,11 +113,13 @@ def cpu_baseline(weights, shape, wl):
             "extrapolated": True}
 
 
-def measured_traffic(kernel: str, workload: str):
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gate_up_traffic.json")
+
+
+def measured_traffic(kernel: str, workload: str, path: str = TRAFFIC_RECORD):
     """HBM bytes per launch of the roofline kernel from the calibrated FETCH_SIZE / WRITE_SIZE
     counter runs recorded in profiles/, or None when there is no record for this kernel and
     workload or the kernel's source has changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "gate_up_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)

@@ -115,7 +115,7 @@ typedef struct rp_round_stats {
   int32_t round_id;
   int32_t n_seqs;
   int32_t decode_steps;
-  int32_t reserved;
+  int32_t kind;            /* 0: plain or short (speculative) round, 1: long round */
   int64_t prompt_tokens;
   int64_t generated_tokens;
   int64_t peak_pages;
@@ -209,6 +209,51 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
                               const int32_t* round_ids, int32_t* resp_tokens_out,
                               rp_round_stats* stats_out, int32_t max_stats,
                               int32_t* n_rounds_out);
+
+/* Tail batching run online on the engine (section 3).  n_prompts prompts,
+ * submitted in order, each with r_spec = ceil(eta * R0) candidate responses;
+ * response r of prompt p is sequence seq_ids[p * r_spec + r] with forced
+ * length max_new_tokens[p * r_spec + r] and its own copy of prompt p.
+ * Rounds follow the policy of rp_plan_tail_batching, but completion is
+ * observed on the engine step by step:
+ *   short round  the next ceil(eta * P0) fresh prompts start all their
+ *                responses together (all must fit max_seqs and the KV pool at
+ *                once, checked for every short round before anything runs:
+ *                RP_ERR_CAPACITY).  When a prompt has R0 finished responses
+ *                and fewer than P0 prompts are accepted, it is accepted with
+ *                those R0 responses (lower response index first on a tie) and
+ *                its other responses are aborted at once.  The round ends
+ *                when P0 prompts are accepted (prompts completing in the same
+ *                step: lower index first); every response still running is
+ *                aborted, its pages freed, and its prompt queued.
+ *   long round   when P0 prompts are queued, or no fresh prompt is left,
+ *                up to P0 of the oldest queued prompts run responses
+ *                0..R0-1 to completion, with no speculation.  They start from
+ *                the prompt again: tokens are keyed by (seed, seq_id,
+ *                position), so the tokens an aborted response had produced
+ *                are produced again.
+ *   seq_ids         host [n_prompts * r_spec], unique
+ *   prompt_tokens   host, CSR over prompts with prompt_offsets [n_prompts + 1]
+ *   resp_tokens_out host [sum max_new_tokens]: response i's tokens at offset
+ *                   sum_{j<i} max_new_tokens[j]; only its first resp_len_out[i]
+ *                   entries are written
+ *   resp_len_out    host [n_prompts * r_spec]: tokens the response generated in
+ *                   the last round it ran in (0 if never launched)
+ *   accept_round_out host [n_prompts]: round that accepted the prompt
+ *   kept_out        host [n_prompts * r_spec]: 1 for the R0 responses kept per prompt
+ *   stats_out       host [max_stats] or NULL: one record per round, round_id =
+ *                   round index, kind 0 short / 1 long; idle time counts each
+ *                   response from the moment it finished or was aborted
+ *   n_rounds_out    host or NULL
+ * The engine must have no live sequences.  Other errors as rp_rollout_generate. */
+rp_status rp_rollout_tail_batched(rp_engine* eng, int32_t n_prompts, int32_t r_spec,
+                                  const int64_t* seq_ids, const int32_t* prompt_tokens,
+                                  const int64_t* prompt_offsets, const int32_t* max_new_tokens,
+                                  uint64_t seed, float temperature, int32_t P0, int32_t R0, float eta,
+                                  int32_t* resp_tokens_out, int32_t* resp_len_out,
+                                  int32_t* accept_round_out, int32_t* kept_out,
+                                  rp_round_stats* stats_out, int32_t max_stats,
+                                  int32_t* n_rounds_out);
 
 /* Tail-batching plan (section 3), host only.  n_prompts prompts, submitted
  * in order, each with r_spec = ceil(eta * R0) candidate responses of known

@@ -12,6 +12,7 @@
 #include <array>
 #include <cmath>
 #include <cstring>
+#include <deque>
 #include <map>
 #include <numeric>
 
@@ -671,16 +672,12 @@ int32_t Engine::get_tokens(int64_t id, int32_t* out, int32_t cap) {
   return q.n_gen;
 }
 
-int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
-                        const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
-                        int32_t* resp_out, rp_round_stats* stats, int32_t max_stats) {
-  if (!order_.empty()) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
-  if (n < 1 || !ids || !toks || !offs || !max_new || !resp_out)
-    throw RpError(RP_ERR_INVALID_ARG, "rollout: null array or n < 1");
+void Engine::validate_seqs(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                           const int32_t* max_new, float temp, std::vector<int64_t>& resp_off) const {
   if (!(temp >= 0.f) || std::isinf(temp)) throw RpError(RP_ERR_INVALID_ARG, "temperature must be finite and >= 0");
   if (offs[0] != 0) throw RpError(RP_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
   std::unordered_map<int64_t, int> seen;
-  std::vector<int64_t> resp_off(n + 1, 0);
+  resp_off.assign(static_cast<size_t>(n) + 1, 0);
   for (int32_t i = 0; i < n; ++i) {
     const int64_t p = offs[i + 1] - offs[i];
     if (p < 1 || max_new[i] < 1) throw RpError(RP_ERR_INVALID_ARG, "prompts and max_new_tokens must be >= 1");
@@ -694,140 +691,300 @@ int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, cons
       if (toks[t] < 0 || toks[t] >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "prompt token id out of range");
     resp_off[i + 1] = resp_off[i] + max_new[i];
   }
-  std::map<int32_t, std::vector<int32_t>> rounds;
-  for (int32_t i = 0; i < n; ++i) rounds[round_ids ? round_ids[i] : 0].push_back(i);
+}
 
+hipEvent_t Engine::event_at(size_t k) {
+  while (events_.size() <= k) {
+    hipEvent_t e;
+    HIP_TRY(hipEventCreate(&e));
+    events_.push_back(e);
+  }
+  return events_[k];
+}
+
+void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, int32_t* resp_out,
+                       int32_t* gen_out, Race* race, rp_round_stats* st) {
   const size_t resp_cap = static_cast<size_t>(lim_.max_seqs) * lim_.max_context;
   int32_t* resp_dev = sp<int32_t>(plan_.resp);
   const int32_t* hist = sp<int32_t>(plan_.hist);
-  auto event_at = [&](size_t k) {
-    while (events_.size() <= k) {
-      hipEvent_t e;
-      HIP_TRY(hipEventCreate(&e));
-      events_.push_back(e);
+  size_t next = 0;
+  size_t n_ev = 0;
+  hipEvent_t ev_start = event_at(n_ev++);
+  hipEvent_t ev_pre = event_at(n_ev++);
+  hipEvent_t ev_end = event_at(n_ev++);
+  std::vector<std::pair<size_t, int32_t>> left_ev;     // (event index, member position) per departure
+  std::vector<std::array<int64_t, 3>> pending_copies;  // dev offset, host offset, length
+  size_t resp_cursor = 0;
+  std::unordered_map<int32_t, int32_t> slot_member;    // slot -> position in members
+  pool_.reset_peak();
+  int32_t steps = 0;
+  int64_t prompt_tokens = 0, gen_tokens = 0;
+
+  // Race bookkeeping: finished members per prompt in completion order, and
+  // whether each prompt has been decided (accepted, or lost the race).
+  std::vector<std::vector<int32_t>> done;
+  std::vector<uint8_t> decided;
+  int32_t n_acc = 0;
+  if (race) {
+    done.resize(race->n_prompts);
+    decided.assign(race->n_prompts, 0);
+    race->accepted.assign(race->n_prompts, 0);
+    race->kept.assign(members.size(), 0);
+  }
+
+  auto flush = [&]() {
+    if (pending_copies.empty()) return;
+    HIP_TRY(hipStreamSynchronize(stream_));
+    for (auto& c : pending_copies)
+      HIP_TRY(hipMemcpy(resp_out + c[1], resp_dev + c[0], static_cast<size_t>(c[2]) * 4, hipMemcpyDeviceToHost));
+    pending_copies.clear();
+    resp_cursor = 0;
+  };
+  auto admit = [&]() {
+    std::vector<int64_t> b_ids, b_offs{0};
+    std::vector<int32_t> b_toks, b_new, b_mem;
+    int64_t pages = 0;
+    while (next < members.size() && b_ids.size() < free_slots_.size()) {
+      const int32_t i = members[next];
+      const int64_t need = PagePool::pages_for(a.offs[i + 1] - a.offs[i] + a.max_new[i] - 1, kPageTokens);
+      if (!pool_.can_take(pages + need)) break;
+      pages += need;
+      b_ids.push_back(a.ids[i]);
+      b_toks.insert(b_toks.end(), a.toks + a.offs[i], a.toks + a.offs[i + 1]);
+      b_offs.push_back(static_cast<int64_t>(b_toks.size()));
+      b_new.push_back(a.max_new[i]);
+      b_mem.push_back(static_cast<int32_t>(next));
+      prompt_tokens += a.offs[i + 1] - a.offs[i];
+      ++next;
     }
-    return events_[k];
+    if (b_ids.empty()) return;
+    const size_t before = order_.size();
+    prefill(static_cast<int32_t>(b_ids.size()), b_ids.data(), b_toks.data(), b_offs.data(), b_new.data(), a.seed,
+            a.temp, nullptr, nullptr);
+    for (size_t k = 0; k < b_mem.size(); ++k) slot_member[order_[before + k]] = b_mem[k];
+  };
+  // Copies a departing sequence's tokens out, then frees its slot and pages.
+  auto retire = [&](int32_t s) {
+    const int32_t k = slot_member.at(s);
+    const int32_t i = members[k];
+    const int64_t len = slots_[s].n_gen;
+    if (resp_cursor + len > resp_cap) flush();
+    HIP_TRY(hipMemcpyAsync(resp_dev + resp_cursor, hist + static_cast<size_t>(s) * lim_.max_context, len * 4,
+                           hipMemcpyDeviceToDevice, stream_));
+    pending_copies.push_back({static_cast<int64_t>(resp_cursor), a.resp_off[i], len});
+    resp_cursor += len;
+    if (gen_out) gen_out[i] = static_cast<int32_t>(len);
+    left_ev.push_back({n_ev, k});
+    gen_tokens += len;
+    slot_member.erase(s);
+    release(s);
+  };
+  auto collect = [&]() {
+    std::vector<int32_t> leaving;
+    std::vector<uint8_t> abort_prompt;
+    bool stop = false;
+    if (race) {
+      // Completions of this step, in member order (responses of a prompt by index).
+      std::vector<int32_t> fresh;
+      for (int32_t s : order_)
+        if (slots_[s].finished) {
+          const int32_t k = slot_member.at(s);
+          const int32_t p = race->prompt[k];
+          if (decided[p]) continue;
+          done[p].push_back(k);
+          if (static_cast<int32_t>(done[p].size()) == race->R0) fresh.push_back(p);
+        }
+      std::sort(fresh.begin(), fresh.end());
+      abort_prompt.assign(race->n_prompts, 0);
+      for (int32_t p : fresh) {
+        decided[p] = 1;
+        if (n_acc < race->keep) {
+          ++n_acc;
+          race->accepted[p] = 1;
+          for (int32_t j = 0; j < race->R0; ++j) race->kept[done[p][j]] = 1;
+          abort_prompt[p] = 1;  // its other responses can no longer be kept
+        }
+      }
+      stop = n_acc >= race->keep;
+    }
+    for (int32_t s : order_) {
+      const bool fin = slots_[s].finished;
+      if (fin || stop || (race && abort_prompt[race->prompt[slot_member.at(s)]])) leaving.push_back(s);
+    }
+    if (leaving.empty()) return;
+    for (int32_t s : leaving) retire(s);
+    HIP_TRY(hipEventRecord(event_at(n_ev), stream_));
+    ++n_ev;
   };
 
+  HIP_TRY(hipEventRecord(ev_start, stream_));
+  admit();
+  if (race && next < members.size())
+    throw RpError(RP_ERR_CAPACITY, "a race round must start all of its responses together");
+  HIP_TRY(hipEventRecord(ev_pre, stream_));
+  collect();
+  while (true) {
+    if (next < members.size()) {
+      admit();
+      collect();
+    }
+    if (order_.empty() && next >= members.size()) break;
+    if (order_.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "rollout: a sequence cannot be admitted");
+    decode_step(nullptr, nullptr, nullptr);
+    ++steps;
+    collect();
+  }
+  HIP_TRY(hipEventRecord(ev_end, stream_));
+  flush();
+  HIP_TRY(hipEventSynchronize(ev_end));
+
+  if (!st) return;
+  const int32_t round_id = st->round_id, kind = st->kind;
+  *st = rp_round_stats{};
+  float ms = 0.f;
+  st->round_id = round_id;
+  st->kind = kind;
+  st->n_seqs = static_cast<int32_t>(members.size());
+  st->decode_steps = steps;
+  st->prompt_tokens = prompt_tokens;
+  st->generated_tokens = gen_tokens;
+  st->peak_pages = pool_.peak_used();
+  HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_end));
+  st->makespan_ms = ms;
+  HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_pre));
+  st->prefill_ms = ms;
+  st->decode_ms = st->makespan_ms - st->prefill_ms;
+  double idle = 0.0;
+  for (auto& le : left_ev) {
+    HIP_TRY(hipEventElapsedTime(&ms, events_[le.first], ev_end));
+    idle += std::max(0.0, static_cast<double>(ms)) * 1e-3;
+  }
+  st->idle_slot_s = idle;
+  const double denom = static_cast<double>(members.size()) * st->makespan_ms * 1e-3;
+  st->slot_idle = denom > 0 ? idle / denom : 0.0;
+}
+
+int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                        const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
+                        int32_t* resp_out, rp_round_stats* stats, int32_t max_stats) {
+  if (!order_.empty()) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
+  if (n < 1 || !ids || !toks || !offs || !max_new || !resp_out)
+    throw RpError(RP_ERR_INVALID_ARG, "rollout: null array or n < 1");
+  std::vector<int64_t> resp_off;
+  validate_seqs(n, ids, toks, offs, max_new, temp, resp_off);
+  std::map<int32_t, std::vector<int32_t>> rounds;
+  for (int32_t i = 0; i < n; ++i) rounds[round_ids ? round_ids[i] : 0].push_back(i);
+  const SeqArrays arr{ids, toks, offs, max_new, resp_off.data(), seed, temp};
   int32_t r_idx = 0;
   for (auto& kv : rounds) {
-    const std::vector<int32_t>& members = kv.second;
-    size_t next = 0;
-    size_t n_ev = 0;
-    hipEvent_t ev_start = event_at(n_ev++);
-    hipEvent_t ev_pre = event_at(n_ev++);
-    hipEvent_t ev_end = event_at(n_ev++);
-    std::vector<std::pair<size_t, int32_t>> finish_ev;  // (event index, member position)
-    std::vector<std::array<int64_t, 3>> pending_copies;  // dev offset, host offset, length
-    size_t resp_cursor = 0;
-    std::unordered_map<int32_t, int32_t> slot_member;
-    pool_.reset_peak();
-    int32_t steps = 0;
-    int64_t prompt_tokens = 0, gen_tokens = 0;
-
-    auto flush = [&]() {
-      if (pending_copies.empty()) return;
-      HIP_TRY(hipStreamSynchronize(stream_));
-      for (auto& c : pending_copies)
-        HIP_TRY(hipMemcpy(resp_out + c[1], resp_dev + c[0], static_cast<size_t>(c[2]) * 4, hipMemcpyDeviceToHost));
-      pending_copies.clear();
-      resp_cursor = 0;
-    };
-    auto admit = [&]() {
-      std::vector<int64_t> b_ids, b_offs{0};
-      std::vector<int32_t> b_toks, b_new, b_mem;
-      int64_t pages = 0;
-      while (next < members.size() && b_ids.size() < free_slots_.size()) {
-        const int32_t i = members[next];
-        const int64_t need = PagePool::pages_for(offs[i + 1] - offs[i] + max_new[i] - 1, kPageTokens);
-        if (!pool_.can_take(pages + need)) break;
-        pages += need;
-        b_ids.push_back(ids[i]);
-        b_toks.insert(b_toks.end(), toks + offs[i], toks + offs[i + 1]);
-        b_offs.push_back(static_cast<int64_t>(b_toks.size()));
-        b_new.push_back(max_new[i]);
-        b_mem.push_back(i);
-        prompt_tokens += offs[i + 1] - offs[i];
-        ++next;
-      }
-      if (b_ids.empty()) return;
-      const size_t before = order_.size();
-      prefill(static_cast<int32_t>(b_ids.size()), b_ids.data(), b_toks.data(), b_offs.data(), b_new.data(), seed,
-              temp, nullptr, nullptr);
-      for (size_t k = 0; k < b_mem.size(); ++k) slot_member[order_[before + k]] = b_mem[k];
-    };
-    auto collect_finished = [&]() {
-      bool any = false;
-      for (int32_t s : order_) {
-        if (!slots_[s].finished) continue;
-        const int32_t i = slot_member.at(s);
-        const int64_t len = max_new[i];
-        if (resp_cursor + len > resp_cap) flush();
-        HIP_TRY(hipMemcpyAsync(resp_dev + resp_cursor, hist + static_cast<size_t>(s) * lim_.max_context, len * 4,
-                               hipMemcpyDeviceToDevice, stream_));
-        pending_copies.push_back({static_cast<int64_t>(resp_cursor), resp_off[i], len});
-        resp_cursor += len;
-        finish_ev.push_back({n_ev, i});
-        gen_tokens += len;
-        any = true;
-      }
-      if (any) {
-        HIP_TRY(hipEventRecord(event_at(n_ev), stream_));
-        ++n_ev;
-        for (int32_t s : std::vector<int32_t>(order_))
-          if (slots_[s].finished) {
-            slot_member.erase(s);
-            release(s);
-          }
-      }
-    };
-
-    HIP_TRY(hipEventRecord(ev_start, stream_));
-    admit();
-    HIP_TRY(hipEventRecord(ev_pre, stream_));
-    collect_finished();
-    while (true) {
-      if (next < members.size()) {
-        admit();
-        collect_finished();
-      }
-      if (order_.empty() && next >= members.size()) break;
-      if (order_.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "rollout: a sequence cannot be admitted");
-      decode_step(nullptr, nullptr, nullptr);
-      ++steps;
-      collect_finished();
-    }
-    HIP_TRY(hipEventRecord(ev_end, stream_));
-    flush();
-    HIP_TRY(hipEventSynchronize(ev_end));
-
-    if (stats && r_idx < max_stats) {
-      rp_round_stats& st = stats[r_idx];
-      st = rp_round_stats{};
-      float ms = 0.f;
-      st.round_id = kv.first;
-      st.n_seqs = static_cast<int32_t>(members.size());
-      st.decode_steps = steps;
-      st.prompt_tokens = prompt_tokens;
-      st.generated_tokens = gen_tokens;
-      st.peak_pages = pool_.peak_used();
-      HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_end));
-      st.makespan_ms = ms;
-      HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_pre));
-      st.prefill_ms = ms;
-      st.decode_ms = st.makespan_ms - st.prefill_ms;
-      double idle = 0.0;
-      for (auto& fe : finish_ev) {
-        HIP_TRY(hipEventElapsedTime(&ms, events_[fe.first], ev_end));
-        idle += std::max(0.0, static_cast<double>(ms)) * 1e-3;
-      }
-      st.idle_slot_s = idle;
-      const double denom = static_cast<double>(members.size()) * st.makespan_ms * 1e-3;
-      st.slot_idle = denom > 0 ? idle / denom : 0.0;
-    }
+    rp_round_stats st{};
+    st.round_id = kv.first;
+    run_round(kv.second, arr, resp_out, nullptr, nullptr, &st);
+    if (stats && r_idx < max_stats) stats[r_idx] = st;
     ++r_idx;
   }
   return r_idx;
+}
+
+int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const int64_t* ids, const int32_t* ptoks,
+                                     const int64_t* poffs, const int32_t* max_new, uint64_t seed, float temp,
+                                     int32_t P0, int32_t R0, float eta, int32_t* resp_out, int32_t* gen_out,
+                                     int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
+                                     int32_t max_stats) {
+  if (!order_.empty()) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
+  if (n_prompts < 1 || r_spec < 1 || !ids || !ptoks || !poffs || !max_new || !resp_out || !gen_out ||
+      !accept_round_out || !kept_out)
+    throw RpError(RP_ERR_INVALID_ARG, "tail-batched rollout: null array or n_prompts < 1");
+  if (P0 < 1 || R0 < 1 || !(eta >= 1.f) || std::isinf(eta))
+    throw RpError(RP_ERR_INVALID_ARG, "tail-batched rollout needs P0 >= 1, R0 >= 1 and a finite eta >= 1");
+  if (r_spec != static_cast<int32_t>(std::ceil(static_cast<double>(eta) * R0 - 1e-9)))
+    throw RpError(RP_ERR_INVALID_ARG, "r_spec must equal ceil(eta * R0)");
+  if (static_cast<int64_t>(n_prompts) * r_spec > (int64_t{1} << 30))
+    throw RpError(RP_ERR_INVALID_ARG, "too many responses");
+  if (poffs[0] != 0) throw RpError(RP_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
+  for (int32_t p = 0; p < n_prompts; ++p)
+    if (poffs[p + 1] < poffs[p]) throw RpError(RP_ERR_INVALID_ARG, "prompt_offsets must be non-decreasing");
+
+  // One sequence per (prompt, response), each with its own copy of the prompt.
+  const int32_t n = n_prompts * r_spec;
+  std::vector<int64_t> offs(static_cast<size_t>(n) + 1, 0);
+  std::vector<int32_t> toks;
+  toks.reserve(static_cast<size_t>(poffs[n_prompts]) * r_spec);
+  for (int32_t p = 0; p < n_prompts; ++p)
+    for (int32_t r = 0; r < r_spec; ++r) {
+      toks.insert(toks.end(), ptoks + poffs[p], ptoks + poffs[p + 1]);
+      offs[static_cast<size_t>(p) * r_spec + r + 1] = static_cast<int64_t>(toks.size());
+    }
+  std::vector<int64_t> resp_off;
+  validate_seqs(n, ids, toks.data(), offs.data(), max_new, temp, resp_off);
+
+  // A short round starts every launched response at once: check that each
+  // one fits before anything runs.
+  const int32_t p_spec = static_cast<int32_t>(std::ceil(static_cast<double>(eta) * P0 - 1e-9));
+  for (int32_t p0 = 0; p0 < n_prompts; p0 += p_spec) {
+    int64_t pages = 0, seqs = 0;
+    for (int32_t p = p0; p < std::min(n_prompts, p0 + p_spec); ++p)
+      for (int32_t r = 0; r < r_spec; ++r) {
+        const size_t i = static_cast<size_t>(p) * r_spec + r;
+        pages += PagePool::pages_for(offs[i + 1] - offs[i] + max_new[i] - 1, kPageTokens);
+        ++seqs;
+      }
+    if (seqs > lim_.max_seqs || pages > pool_.capacity())
+      throw RpError(RP_ERR_CAPACITY, "a short round's responses do not fit max_seqs or the KV pool together");
+  }
+
+  const SeqArrays arr{ids, toks.data(), offs.data(), max_new, resp_off.data(), seed, temp};
+  for (int32_t p = 0; p < n_prompts; ++p) accept_round_out[p] = -1;
+  for (int32_t i = 0; i < n; ++i) kept_out[i] = 0, gen_out[i] = 0;
+  std::deque<int32_t> queue;  // prompts aborted by short rounds, oldest first
+  int32_t next_fresh = 0, k = 0;
+  while (next_fresh < n_prompts || !queue.empty()) {
+    rp_round_stats st{};
+    st.round_id = k;
+    std::vector<int32_t> launched, members;
+    if (static_cast<int32_t>(queue.size()) >= P0 || (next_fresh >= n_prompts && !queue.empty())) {
+      // Long round: the oldest queued prompts, R0 responses each, no speculation.
+      st.kind = 1;
+      while (!queue.empty() && static_cast<int32_t>(launched.size()) < P0) {
+        launched.push_back(queue.front());
+        queue.pop_front();
+      }
+      std::sort(launched.begin(), launched.end());
+      for (int32_t p : launched)
+        for (int32_t r = 0; r < R0; ++r) members.push_back(p * r_spec + r);
+      run_round(members, arr, resp_out, gen_out, nullptr, &st);
+      for (int32_t p : launched) {
+        accept_round_out[p] = k;
+        for (int32_t r = 0; r < R0; ++r) kept_out[p * r_spec + r] = 1;
+      }
+    } else {
+      // Short round: race to completion among the next ceil(eta * P0) fresh prompts.
+      st.kind = 0;
+      for (int32_t j = 0; j < p_spec && next_fresh < n_prompts; ++j) launched.push_back(next_fresh++);
+      Race race;
+      race.n_prompts = static_cast<int32_t>(launched.size());
+      race.R0 = R0;
+      race.keep = std::min(P0, race.n_prompts);
+      for (int32_t j = 0; j < race.n_prompts; ++j)
+        for (int32_t r = 0; r < r_spec; ++r) {
+          members.push_back(launched[j] * r_spec + r);
+          race.prompt.push_back(j);
+        }
+      run_round(members, arr, resp_out, gen_out, &race, &st);
+      for (int32_t j = 0; j < race.n_prompts; ++j) {
+        const int32_t p = launched[j];
+        if (race.accepted[j]) {
+          accept_round_out[p] = k;
+          for (int32_t r = 0; r < r_spec; ++r) kept_out[p * r_spec + r] = race.kept[j * r_spec + r];
+        } else {
+          queue.push_back(p);
+        }
+      }
+    }
+    if (stats && k < max_stats) stats[k] = st;
+    ++k;
+  }
+  return k;
 }
 
 }  // namespace rollpack

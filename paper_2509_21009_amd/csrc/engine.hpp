@@ -48,8 +48,25 @@ struct Seq {
   std::vector<int32_t> pages;
 };
 
-struct RoundInput {
-  std::vector<int32_t> idx;  // indices into the call's arrays
+// Per-sequence inputs of one rollout call (prompt CSR per sequence).
+struct SeqArrays {
+  const int64_t* ids;
+  const int32_t* toks;
+  const int64_t* offs;
+  const int32_t* max_new;
+  const int64_t* resp_off;  // [n + 1] token offsets into the response buffer
+  uint64_t seed;
+  float temp;
+};
+
+// Race-to-completion state of a short round (section 3): members are the
+// responses of n_prompts prompts; the first `keep` prompts with R0 finished
+// responses are accepted, each keeping its first R0 finished responses.
+struct Race {
+  std::vector<int32_t> prompt;     // [members] prompt (0..n_prompts-1) of each member
+  int32_t n_prompts = 0, R0 = 1, keep = 1;
+  std::vector<uint8_t> accepted;   // [n_prompts] out
+  std::vector<uint8_t> kept;       // [members] out
 };
 
 class Engine {
@@ -67,6 +84,11 @@ class Engine {
   int32_t rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
                   const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
                   int32_t* resp_out, rp_round_stats* stats, int32_t max_stats);
+  int32_t rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const int64_t* ids, const int32_t* ptoks,
+                               const int64_t* poffs, const int32_t* max_new, uint64_t seed, float temp,
+                               int32_t P0, int32_t R0, float eta, int32_t* resp_out, int32_t* gen_out,
+                               int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
+                               int32_t max_stats);
 
   void profile_enable(uint32_t mask);
   int32_t profile_read(rp_kernel_stats* out, int32_t cap);
@@ -91,6 +113,15 @@ class Engine {
   void run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t* toks, const int64_t* offs,
                          const std::vector<int32_t>& seq_index, float* logits_out);
   void release(int32_t slot);
+  void validate_seqs(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                     const int32_t* max_new, float temp, std::vector<int64_t>& resp_off) const;
+  hipEvent_t event_at(size_t k);
+  // Runs one round over `members` (indices into a) to its end: admits them
+  // (in waves when the pool is short, all at once for a race), decodes, and
+  // copies each departing sequence's tokens to resp_out.  With a race the
+  // round ends when race->keep prompts are accepted and the rest are aborted.
+  void run_round(const std::vector<int32_t>& members, const SeqArrays& a, int32_t* resp_out, int32_t* gen_out,
+                 Race* race, rp_round_stats* st);
   template <typename T> T* sp(size_t off) const { return reinterpret_cast<T*>(scratch_ + off); }
 
   rp_model_config cfg_;

@@ -143,6 +143,21 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
   });
 }
 
+rp_status rp_rollout_tail_batched(rp_engine* eng, int32_t n_prompts, int32_t r_spec, const int64_t* seq_ids,
+                                  const int32_t* prompt_tokens, const int64_t* prompt_offsets,
+                                  const int32_t* max_new_tokens, uint64_t seed, float temperature, int32_t P0,
+                                  int32_t R0, float eta, int32_t* resp_tokens_out, int32_t* resp_len_out,
+                                  int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats_out,
+                                  int32_t max_stats, int32_t* n_rounds_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    if (max_stats < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "max_stats must be >= 0");
+    const int32_t r = e->rollout_tail_batched(n_prompts, r_spec, seq_ids, prompt_tokens, prompt_offsets,
+                                              max_new_tokens, seed, temperature, P0, R0, eta, resp_tokens_out,
+                                              resp_len_out, accept_round_out, kept_out, stats_out, max_stats);
+    if (n_rounds_out) *n_rounds_out = r;
+  });
+}
+
 rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens, int32_t P0, int32_t R0,
                                 float eta, int32_t max_rounds, int32_t cap_launch, int32_t* round_kind_out,
                                 int32_t* round_time_out, int32_t* launch_off_out, int32_t* launch_prompt_out,

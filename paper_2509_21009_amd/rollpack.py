@@ -47,13 +47,13 @@ class RpEngineLimits(ctypes.Structure):
 
 class RpRoundStats(ctypes.Structure):
     _fields_ = [("round_id", ctypes.c_int32), ("n_seqs", ctypes.c_int32), ("decode_steps", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("prompt_tokens", ctypes.c_int64),
+                ("kind", ctypes.c_int32), ("prompt_tokens", ctypes.c_int64),
                 ("generated_tokens", ctypes.c_int64), ("peak_pages", ctypes.c_int64),
                 ("makespan_ms", ctypes.c_double), ("prefill_ms", ctypes.c_double),
                 ("decode_ms", ctypes.c_double), ("slot_idle", ctypes.c_double), ("idle_slot_s", ctypes.c_double)]
 
     def as_dict(self) -> dict:
-        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
+        return {f: getattr(self, f) for f, _ in self._fields_}
 
 
 KERNEL_CLASSES = ("embed_norm", "add_norm", "gemm_qkv", "rope_append", "attn", "attn_merge", "gemm_o",
@@ -98,6 +98,10 @@ SIGNATURES = {
     "rp_rollout_generate": (ctypes.c_int, [_P, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P, ctypes.c_uint64,
                                            ctypes.c_float, _I32P, _I32P, ctypes.POINTER(RpRoundStats),
                                            ctypes.c_int32, _I32P]),
+    "rp_rollout_tail_batched": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P,
+                                               ctypes.c_uint64, ctypes.c_float, ctypes.c_int32, ctypes.c_int32,
+                                               ctypes.c_float, _I32P, _I32P, _I32P, _I32P,
+                                               ctypes.POINTER(RpRoundStats), ctypes.c_int32, _I32P]),
     "rp_plan_tail_batching": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_int32, ctypes.c_int32,
                                              ctypes.c_float, ctypes.c_int32, ctypes.c_int32, _I32P, _I32P, _I32P,
                                              _I32P, _I32P, _I32P, _I32P, _I32P]),
@@ -222,6 +226,32 @@ def rp_rollout_generate(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_ne
                                               ctypes.c_float(temperature), rid_p, resp.ctypes.data_as(_I32P), stats,
                                               max_stats, ctypes.byref(nr)))
     return resp, [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
+
+
+def rp_rollout_tail_batched(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed: int,
+                            temperature: float, P0: int, R0: int, eta: float, max_stats: int = 0):
+    """seq_ids, max_new_tokens: [n_prompts, r_spec]; prompt CSR over prompts.
+
+    Returns (resp_tokens, resp_len [n, r_spec], accept_round [n], kept [n, r_spec] bool, round stats)."""
+    ids = np.ascontiguousarray(seq_ids, np.int64)
+    n, r_spec = ids.shape
+    toks, toks_p = _arr(prompt_tokens, np.int32)
+    offs, offs_p = _arr(prompt_offsets, np.int64)
+    mn = np.ascontiguousarray(max_new_tokens, np.int32)
+    assert mn.shape == ids.shape and len(offs) == n + 1
+    max_stats = max_stats or 2 * n + 2
+    resp = np.zeros(max(int(mn.sum()), 1), np.int32)
+    glen = np.zeros((n, r_spec), np.int32)
+    acc = np.zeros(n, np.int32)
+    kept = np.zeros((n, r_spec), np.int32)
+    stats = (RpRoundStats * max_stats)()
+    nr = ctypes.c_int32()
+    P = lambda a: a.ctypes.data_as(_I32P)  # noqa: E731
+    _check(load_library().rp_rollout_tail_batched(eng, n, r_spec, ids.ctypes.data_as(_I64P), toks_p, offs_p, P(mn),
+                                                  ctypes.c_uint64(seed), ctypes.c_float(temperature), P0, R0,
+                                                  ctypes.c_float(eta), P(resp), P(glen), P(acc), P(kept), stats,
+                                                  max_stats, ctypes.byref(nr)))
+    return resp, glen, acc, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
 
 
 def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float):
@@ -360,6 +390,12 @@ class Engine:
     def rollout(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature, round_ids=None):
         return rp_rollout_generate(self.handle, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
                                    temperature, round_ids)
+
+
+    def rollout_tail_batched(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
+                             P0: int, R0: int, eta: float):
+        return rp_rollout_tail_batched(self.handle, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
+                                       temperature, P0, R0, eta)
 
 
 def weights_for_engine(w: dict) -> dict:

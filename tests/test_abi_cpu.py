@@ -149,12 +149,55 @@ def test_workload_shapes_follow_the_configs():
     assert c2.n == 256 and len(set(c2.prompt_group.tolist())) == 32
 
 
-def test_bench_reports_counter_traffic_only_for_the_measured_kernel():
-    """roofline.traffic comes from the calibrated counter record in profiles/ and is dropped
-    when the workload differs or the kernel source no longer matches the recorded hash."""
+def test_rl_batch_lengths_are_prompt_correlated():
+    from workloads import SHAPES, make_rl_batch
+    s = SHAPES["qwen2.5-0.5b"]
+    kw = dict(p_lo=64, p_hi=512, median=512, lo=32, hi=4096, seed=7)
+    a = make_rl_batch(s, 200, 10, sigma_p=0.6, sigma_r=0.53, **kw)
+    b = make_rl_batch(s, 200, 10, sigma_p=0.6, sigma_r=0.53, **kw)
+    assert np.array_equal(a.max_new, b.max_new) and np.array_equal(a.prompt_tokens, b.prompt_tokens)
+    assert a.max_new.min() >= 32 and a.max_new.max() <= 4096
+    assert len(set(a.seq_ids.reshape(-1).tolist())) == 2000
+    same = make_rl_batch(s, 50, 4, sigma_p=0.6, sigma_r=0.0, **kw)      # no per-response spread
+    assert (same.max_new == same.max_new[:, :1]).all()
+    # log-length variance splits into a between-prompt part (~sigma_p^2) and a within part (~sigma_r^2)
+    lg = np.log(make_rl_batch(s, 2000, 10, sigma_p=0.6, sigma_r=0.53, p_lo=64, p_hi=512, median=512, lo=1,
+                              hi=10**7, seed=8).max_new)
+    within = lg.var(axis=1, ddof=1).mean()
+    between = lg.mean(axis=1).var(ddof=1) - within / 10
+    assert abs(within - 0.53 ** 2) < 0.03 and abs(between - 0.6 ** 2) < 0.05
+    # sequences(): prompt-major, each response with its own prompt's ids
+    w = a.sequences([3, 5], 2)
+    assert w.seq_ids.tolist() == [30, 31, 50, 51] and w.max_new.tolist() == [a.max_new[3, 0], a.max_new[3, 1],
+                                                                             a.max_new[5, 0], a.max_new[5, 1]]
+    assert np.array_equal(w.prompt(2), a.prompt_tokens[a.prompt_offsets[5]:a.prompt_offsets[6]])
+
+
+def test_tail_batched_rollout_rejects_null_engine(lib):
+    with pytest.raises(rp.RollpackError) as e:
+        rp.rp_rollout_tail_batched(None, np.zeros((2, 2), np.int64), np.arange(4, dtype=np.int32),
+                                   np.array([0, 2, 4], np.int64), np.ones((2, 2), np.int32), 0, 1.0, 1, 2, 1.0)
+    assert e.value.status == 1
+
+
+def test_bench_reports_counter_traffic_only_for_the_measured_kernel(tmp_path):
+    """roofline.traffic comes from a calibrated counter record and is dropped when the workload
+    or kernel differs or the kernel source no longer matches the recorded hash."""
+    import hashlib
     import json
     import bench
-    rec = json.load(open(os.path.join(ROOT, "profiles", "gate_up_traffic.json")))
-    assert bench.measured_traffic("gemm_gate_up", "7b-long") == rec["traffic_bytes_per_launch"]
-    assert bench.measured_traffic("gemm_gate_up", "7b-short") is None
-    assert bench.measured_traffic("gemm_down", "7b-long") is None
+    src = "paper_2509_21009_amd/csrc/k_gemm.hip"
+    digest = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
+    rec = {"kernel": "gemm_gate_up", "workload": "7b-long", "source": src, "source_sha256": digest,
+           "traffic_bytes_per_launch": 123456}
+    path = tmp_path / "rec.json"
+    path.write_text(json.dumps(rec))
+    assert bench.measured_traffic("gemm_gate_up", "7b-long", str(path)) == 123456
+    assert bench.measured_traffic("gemm_gate_up", "7b-short", str(path)) is None
+    assert bench.measured_traffic("gemm_down", "7b-long", str(path)) is None
+    path.write_text(json.dumps(dict(rec, source_sha256="0" * 64)))
+    assert bench.measured_traffic("gemm_gate_up", "7b-long", str(path)) is None
+    assert bench.measured_traffic("gemm_gate_up", "7b-long", str(tmp_path / "missing.json")) is None
+    # the committed record names the kernel bench.py reports by default
+    committed = json.load(open(bench.TRAFFIC_RECORD))
+    assert committed["kernel"] == "gemm_gate_up" and committed["workload"] == "7b-long"

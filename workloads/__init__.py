@@ -7,9 +7,11 @@ is imported here.
 """
 from .gen import (  # noqa: F401
     ModelShape,
+    RLBatch,
     SHAPES,
     Workload,
     WORKLOADS,
+    make_rl_batch,
     make_weights,
     make_workload,
     tensor_names,

@@ -241,3 +241,60 @@ def make_workload(name: str, shape: Optional[ModelShape] = None) -> Workload:
 
 
 WORKLOADS = ("tiny", "0.5b", "7b-short", "7b-long", "7b-mixed", "32b")
+
+
+@dataclasses.dataclass
+class RLBatch:
+    """Prompts of consecutive RL steps, each with r_spec candidate responses.
+
+    Response r of prompt p is sequence ``seq_ids[p, r]`` with forced length
+    ``max_new[p, r]``.  Prompt ids are stored once per prompt (CSR)."""
+    name: str
+    shape: ModelShape
+    seq_ids: np.ndarray         # int64 [n_prompts, r_spec], unique
+    prompt_tokens: np.ndarray   # int32 [sum p]
+    prompt_offsets: np.ndarray  # int64 [n_prompts + 1]
+    max_new: np.ndarray         # int32 [n_prompts, r_spec]
+    temperature: float
+    sample_seed: int
+
+    @property
+    def n_prompts(self) -> int:
+        return self.seq_ids.shape[0]
+
+    @property
+    def r_spec(self) -> int:
+        return self.seq_ids.shape[1]
+
+    def sequences(self, prompts, responses: int) -> Workload:
+        """The first `responses` responses of the given prompts, one sequence each (prompt-major)."""
+        prompts = [int(p) for p in prompts]
+        idx = [(p, r) for p in prompts for r in range(responses)]
+        seq_prompts = [self.prompt_tokens[self.prompt_offsets[p]:self.prompt_offsets[p + 1]] for p, _ in idx]
+        offs = np.zeros(len(idx) + 1, np.int64)
+        offs[1:] = np.cumsum([len(t) for t in seq_prompts])
+        return Workload(self.name, self.shape, np.array([self.seq_ids[p, r] for p, r in idx], np.int64),
+                        np.concatenate(seq_prompts).astype(np.int32), offs,
+                        np.array([self.max_new[p, r] for p, r in idx], np.int32),
+                        np.array([p for p, _ in idx], np.int32), self.temperature, self.sample_seed)
+
+
+def make_rl_batch(shape: ModelShape, n_prompts: int, r_spec: int, *, p_lo: int, p_hi: int, median: float,
+                  sigma_p: float, sigma_r: float, lo: int, hi: int, seed: int, sample_seed: int = 0,
+                  temperature: float = 1.0, name: str = "rl") -> RLBatch:
+    """Prompt-correlated long-tail lengths: log L = log median + sigma_p z_p + sigma_r z_pr, clamped to [lo, hi].
+
+    z_p is one standard normal draw per prompt (its difficulty: hard prompts give
+    long responses across the board, as the paper observes in section 6.3) and
+    z_pr one per response.  Prompt lengths are U[p_lo, p_hi], ids U[0, vocab)."""
+    rng = np.random.Generator(np.random.Philox(seed))
+    plen = rng.integers(p_lo, p_hi + 1, size=n_prompts)
+    prompts = [rng.integers(0, shape.vocab, size=int(p)).astype(np.int32) for p in plen]
+    z_p = rng.standard_normal(n_prompts)[:, None]
+    z_pr = rng.standard_normal((n_prompts, r_spec))
+    lens = np.clip(np.rint(median * np.exp(sigma_p * z_p + sigma_r * z_pr)), lo, hi).astype(np.int32)
+    offs = np.zeros(n_prompts + 1, np.int64)
+    offs[1:] = np.cumsum(plen)
+    ids = np.arange(n_prompts * r_spec, dtype=np.int64).reshape(n_prompts, r_spec)
+    return RLBatch(name, shape, ids, np.concatenate(prompts).astype(np.int32) if prompts else np.zeros(0, np.int32),
+                   offs, lens, temperature, sample_seed)
