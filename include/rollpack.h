@@ -99,7 +99,8 @@ typedef struct rp_weights {
 
 typedef struct rp_engine_limits {
   int32_t max_seqs;            /* sequences live at once (KV slots), >= 1 */
-  int32_t max_prefill_tokens;  /* prompt tokens per prefill chunk, >= longest prompt */
+  int32_t max_prefill_tokens;  /* tokens per prefill chunk; a longer prompt is prefilled in
+                                  pieces that continue at their positions */
   int32_t max_context;         /* longest prompt + response, <= 65536 */
   int32_t page_tokens;         /* tokens per KV page; must be 64 */
   int64_t kv_pages;            /* pages in the KV pool */
@@ -124,6 +125,8 @@ typedef struct rp_round_stats {
   double decode_ms;
   double slot_idle;        /* in [0, 1] */
   double idle_slot_s;      /* sum over sequences of (round end - own finish), seconds */
+  int64_t preemptions;     /* sequences preempted during the round (RP_KV_ON_DEMAND) */
+  int64_t recomputed_tokens; /* tokens re-prefilled to resume them */
 } rp_round_stats;
 
 /* Bytes of the caller-provided KV pool and scratch workspace for this model
@@ -158,8 +161,9 @@ void rp_engine_destroy(rp_engine* eng);
  *                   temperature 0 is greedy
  *   logits_out      DEVICE [n, V] fp32 or NULL: logits of each prompt's last position
  *   first_tokens_out HOST [n] or NULL: the sampled first tokens (synchronises)
- * KV pages for prompt + max_new_tokens - 1 positions are reserved at
- * admission; RP_ERR_OUT_OF_PAGES if the pool cannot hold them. */
+ * Under RP_KV_RESERVE, KV pages for prompt + max_new_tokens - 1 positions
+ * are reserved at admission; under RP_KV_ON_DEMAND only the prompt's pages
+ * are taken.  RP_ERR_OUT_OF_PAGES if the pool cannot hold them. */
 rp_status rp_prefill(rp_engine* eng, int32_t n, const int64_t* seq_ids,
                      const int32_t* prompt_tokens, const int64_t* prompt_offsets,
                      const int32_t* max_new_tokens, uint64_t seed, float temperature,
@@ -174,7 +178,13 @@ rp_status rp_prefill(rp_engine* eng, int32_t n, const int64_t* seq_ids,
  *   row_ids_out     HOST [max_seqs] or NULL: the sequence id of each row
  *   n_active_out    HOST, the number of rows in this step (0: nothing to do)
  * A sequence that reaches its max_new_tokens becomes finished and keeps its
- * pages until rp_free_finished. */
+ * pages until rp_free_finished.
+ * Under RP_KV_ON_DEMAND the step first resumes preempted sequences that fit
+ * (oldest arrival first; each is recomputed by a prefill of its prompt and
+ * generated tokens, which samples its next token, so it is not among this
+ * step's rows), then gives each row a page for its next position, preempting
+ * the latest-arrived rows while the pool is short.  forced_tokens must be
+ * NULL under that policy. */
 rp_status rp_decode_step(rp_engine* eng, const int32_t* forced_tokens, float* logits_out,
                          int64_t* row_ids_out, int32_t* n_active_out);
 
@@ -183,11 +193,12 @@ rp_status rp_decode_step(rp_engine* eng, const int32_t* forced_tokens, float* lo
 rp_status rp_free_finished(rp_engine* eng, int64_t* finished_ids_out, int32_t cap,
                            int32_t* n_finished_out);
 
-/* Stop live sequences now (speculative abort, section 3) and release them. */
+/* Stop live (or preempted) sequences now (speculative abort, section 3) and
+ * release them. */
 rp_status rp_abort(rp_engine* eng, int32_t n, const int64_t* seq_ids);
 
-/* Copy the generated tokens of a live sequence to host out [cap]; len_out
- * gets the number generated so far.  Synchronises the stream. */
+/* Copy the generated tokens of a live (or preempted) sequence to host out
+ * [cap]; len_out gets the number generated so far.  Synchronises the stream. */
 rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t cap,
                         int32_t* len_out);
 
@@ -211,12 +222,12 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
                               int32_t* n_rounds_out);
 
 /* Tail batching run online on the engine (section 3).  n_prompts prompts,
- * submitted in order, each with r_spec = ceil(eta * R0) candidate responses;
+ * submitted in order, each with r_spec = ceil(eta_r * R0) candidate responses;
  * response r of prompt p is sequence seq_ids[p * r_spec + r] with forced
  * length max_new_tokens[p * r_spec + r] and its own copy of prompt p.
  * Rounds follow the policy of rp_plan_tail_batching, but completion is
  * observed on the engine step by step:
- *   short round  the next ceil(eta * P0) fresh prompts start all their
+ *   short round  the next ceil(eta_p * P0) fresh prompts start all their
  *                responses together (all must fit max_seqs and the KV pool at
  *                once, checked for every short round before anything runs:
  *                RP_ERR_CAPACITY).  When a prompt has R0 finished responses
@@ -249,37 +260,60 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
 rp_status rp_rollout_tail_batched(rp_engine* eng, int32_t n_prompts, int32_t r_spec,
                                   const int64_t* seq_ids, const int32_t* prompt_tokens,
                                   const int64_t* prompt_offsets, const int32_t* max_new_tokens,
-                                  uint64_t seed, float temperature, int32_t P0, int32_t R0, float eta,
+                                  uint64_t seed, float temperature, int32_t P0, int32_t R0,
+                                  float eta_p, float eta_r,
                                   int32_t* resp_tokens_out, int32_t* resp_len_out,
                                   int32_t* accept_round_out, int32_t* kept_out,
                                   rp_round_stats* stats_out, int32_t max_stats,
                                   int32_t* n_rounds_out);
 
 /* Tail-batching plan (section 3), host only.  n_prompts prompts, submitted
- * in order, each with r_spec = ceil(eta * R0) candidate responses of known
- * lengths lens[p * r_spec + r] (decode steps).  A short round launches the
- * next ceil(eta * P0) fresh prompts and keeps the first P0 to have R0
- * finished responses (ties: lower index), each with its R0 shortest
+ * in order, each with r_spec = ceil(eta_r * R0) candidate responses of known
+ * lengths lens[p * r_spec + r], counted in generation steps of one token
+ * each (the first token is the prefill's sample).  eta_p and eta_r are the
+ * speculation factors for prompts and responses (section 6.3 varies them
+ * separately; a product within one part in 10^6 of an integer counts as that
+ * integer).  A short round launches the next ceil(eta_p * P0) fresh prompts
+ * and keeps the first P0 to have R0 finished responses (ties: lower index), each with its R0 shortest
  * responses; the round ends when its P0-th prompt completes and the other
  * prompts join a FIFO long-prompt queue.  When the queue holds P0 prompts,
  * or no fresh prompt is left, a long round runs up to P0 queued prompts with
  * R0 responses each and no speculation.
  *   round_kind_out  host [max_rounds]: 0 short, 1 long
- *   round_time_out  host [max_rounds]: round length in decode steps
+ *   round_time_out  host [max_rounds]: round length in generation steps (an
+ *                   engine runs it in round_time - 1 decode steps)
  *   launch_off_out  host [max_rounds + 1]: CSR offsets into launch_prompt_out
  *   launch_prompt_out host [cap_launch]: prompts launched per round, ascending
- *   run_steps_out   host [cap_launch * r_spec]: steps each launched response ran
+ *   run_steps_out   host [cap_launch * r_spec]: tokens each launched response generated
  *                   (responses r >= R0 of a long round run 0 steps)
  *   accept_round_out host [n_prompts]: round that accepted each prompt
  *   kept_out        host [n_prompts * r_spec]: 1 if the response is kept
  *   n_rounds_out    host */
 rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens,
-                                int32_t P0, int32_t R0, float eta, int32_t max_rounds,
+                                int32_t P0, int32_t R0, float eta_p, float eta_r, int32_t max_rounds,
                                 int32_t cap_launch, int32_t* round_kind_out,
                                 int32_t* round_time_out, int32_t* launch_off_out,
                                 int32_t* launch_prompt_out, int32_t* run_steps_out,
                                 int32_t* accept_round_out, int32_t* kept_out,
                                 int32_t* n_rounds_out);
+
+/* KV page policy of an engine (section 4.2: KV memory pressure causes
+ * preemptions, and their count is the pressure signal). */
+typedef enum rp_kv_policy {
+  RP_KV_RESERVE = 0,    /* reserve every page a sequence will need at admission (default) */
+  RP_KV_ON_DEMAND = 1   /* take a page when a sequence's context crosses into it; when
+                           none is free, preempt the latest-arrived running sequence and
+                           later resume it by recomputing its KV from its tokens */
+} rp_kv_policy;
+
+/* Set the KV page policy (rp_kv_policy).  The engine must have no live or
+ * preempted sequences (RP_ERR_BAD_STATE). */
+rp_status rp_set_kv_policy(rp_engine* eng, int32_t policy);
+
+/* Pool and scheduler state; every output is nullable.  Counters accumulate
+ * over the engine's life. */
+rp_status rp_kv_status(rp_engine* eng, int64_t* free_pages, int32_t* running,
+                       int32_t* waiting, int64_t* preemptions, int64_t* recomputed_tokens);
 
 /* Kernel classes of the rollout step, for rp_profile_* (bit i of a mask = class i). */
 typedef enum rp_kernel_class {

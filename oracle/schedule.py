@@ -1,8 +1,9 @@
 """Tail-batching round policy, simulated on forced lengths -- oracle, test infrastructure only.
 
 Paper section 3 ("Tail Batching"): each rollout step needs P0 prompts with R0
-responses each.  A short round launches ceil(eta*P0) prompts with
-ceil(eta*R0) responses each and keeps only the first P0 prompts to complete,
+responses each.  A short round launches ceil(eta_p*P0) prompts with
+ceil(eta_r*R0) responses each (section 6.3 sets the two factors separately;
+section 3 uses one eta for both) and keeps only the first P0 prompts to complete,
 each with its first R0 responses to complete ("race to completion").  Prompts
 aborted in a short round join a FIFO long-prompt queue; once the queue holds
 P0 prompts they run as a long round with speculation disabled, so every
@@ -18,12 +19,20 @@ responses have.  Readings for cases the paper leaves open:
   * when fewer than ceil(eta*P0) fresh prompts remain, the short round
     launches what is left and keeps min(P0, launched) of them;
   * when no fresh prompt remains, queued prompts are flushed in long rounds
-    of up to P0 prompts.
+    of up to P0 prompts;
+  * a product eta*k within one part in 10^6 of an integer counts as that
+    integer (eta = 1.1 and k = 10 launch 11, not 12).
 """
 from __future__ import annotations
 
 import math
-from typing import Dict, List, Sequence
+from typing import Dict, List, Optional, Sequence
+
+
+def spec_count(eta: float, k: int) -> int:
+    """ceil(eta * k), reading products within 1e-6 relative of an integer as that integer."""
+    x = eta * k
+    return math.ceil(x - 1e-6 * x)
 
 
 def _kth_smallest(vals: Sequence[int], k: int) -> int:
@@ -36,8 +45,8 @@ def _first_k(vals: Sequence[int], k: int) -> List[int]:
 
 
 def short_round(lens: Sequence[Sequence[int]], launched: List[int], P0: int, R0: int,
-                eta: float) -> Dict:
-    r_spec = math.ceil(eta * R0)
+                eta_r: float) -> Dict:
+    r_spec = spec_count(eta_r, R0)
     done_at = {p: _kth_smallest(lens[p][:r_spec], R0) for p in launched}
     keep_n = min(P0, len(launched))
     order = sorted(launched, key=lambda p: (done_at[p], p))
@@ -61,9 +70,12 @@ def long_round(lens: Sequence[Sequence[int]], prompts: List[int], R0: int) -> Di
             "time": max(run.values(), default=0), "run": run}
 
 
-def plan_tail_batching(lens: Sequence[Sequence[int]], P0: int, R0: int, eta: float) -> List[Dict]:
-    """Rounds for prompts 0..n-1 submitted in order; lens[p] holds >= ceil(eta*R0) lengths."""
-    p_spec = math.ceil(eta * P0)
+def plan_tail_batching(lens: Sequence[Sequence[int]], P0: int, R0: int, eta: float,
+                       eta_r: Optional[float] = None) -> List[Dict]:
+    """Rounds for prompts 0..n-1 submitted in order; lens[p] holds >= ceil(eta_r*R0) lengths.
+    eta is the prompt factor eta_p and, unless eta_r is given, the response factor too."""
+    eta_r = eta if eta_r is None else eta_r
+    p_spec = spec_count(eta, P0)
     fresh = list(range(len(lens)))
     queue: List[int] = []
     rounds = []
@@ -73,7 +85,7 @@ def plan_tail_batching(lens: Sequence[Sequence[int]], P0: int, R0: int, eta: flo
             rounds.append(long_round(lens, take, R0))
             continue
         launched, fresh = fresh[:p_spec], fresh[p_spec:]
-        rnd = short_round(lens, launched, P0, R0, eta)
+        rnd = short_round(lens, launched, P0, R0, eta_r)
         queue.extend(rnd["rejected"])
         rounds.append(rnd)
     return rounds

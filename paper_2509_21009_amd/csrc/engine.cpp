@@ -7,6 +7,7 @@
 // All device work is enqueued on one stream; per-step metadata is O(rows)
 // integers copied from pinned staging buffers.
 #include "engine.hpp"
+#include "tail_batch.hpp"
 
 #include <algorithm>
 #include <array>
@@ -232,16 +233,35 @@ void Engine::check_admission(int32_t n, const int64_t* ids, const int64_t* offs,
   for (int32_t i = 0; i < n; ++i) {
     const int64_t p = offs[i + 1] - offs[i];
     if (p < 1) throw RpError(RP_ERR_INVALID_ARG, "every prompt needs at least one token");
-    if (p > lim_.max_prefill_tokens) throw RpError(RP_ERR_CAPACITY, "prompt longer than max_prefill_tokens");
     if (max_new[i] < 1) throw RpError(RP_ERR_INVALID_ARG, "max_new_tokens must be >= 1");
     if (p + max_new[i] - 1 > lim_.max_context) throw RpError(RP_ERR_CAPACITY, "prompt + max_new_tokens - 1 exceeds max_context");
-    if (id2slot_.count(ids[i]) || seen.count(ids[i])) throw RpError(RP_ERR_DUPLICATE_ID, "sequence id already live");
+    if (known_id(ids[i]) || seen.count(ids[i])) throw RpError(RP_ERR_DUPLICATE_ID, "sequence id already live");
     seen[ids[i]] = 1;
     for (int64_t t = offs[i]; t < offs[i + 1]; ++t)
       if (toks[t] < 0 || toks[t] >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "prompt token id out of range");
-    pages += PagePool::pages_for(p + max_new[i] - 1, kPageTokens);
+    if (PagePool::pages_for(p + max_new[i] - 1, kPageTokens) > pool_.capacity())
+      throw RpError(RP_ERR_OUT_OF_PAGES, "a sequence needs more pages than the pool holds");
+    pages += admit_pages(p, max_new[i], p);
   }
   if (!pool_.can_take(pages)) throw RpError(RP_ERR_OUT_OF_PAGES, "KV pool cannot hold the admitted sequences");
+}
+
+int64_t Engine::admit_pages(int64_t prompt_len, int64_t max_new, int64_t ntok) const {
+  return kv_policy_ == RP_KV_RESERVE ? PagePool::pages_for(prompt_len + max_new - 1, kPageTokens)
+                                     : PagePool::pages_for(ntok, kPageTokens);
+}
+
+bool Engine::known_id(int64_t id) const {
+  if (id2slot_.count(id)) return true;
+  for (const Waiting& w : waiting_)
+    if (w.id == id) return true;
+  return false;
+}
+
+Waiting* Engine::find_waiting(int64_t id) {
+  for (Waiting& w : waiting_)
+    if (w.id == id) return &w;
+  return nullptr;
 }
 
 template <typename F>
@@ -411,11 +431,10 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
   launch_timed(RP_K_SAMPLE, static_cast<double>(m_lm) * V * 4, 0, [&] { return launch_sample(sa, s); });
 }
 
-void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t* toks, const int64_t* offs,
-                               const std::vector<int32_t>& seq_index, float* logits_out) {
-  const int n = static_cast<int>(slots.size());
+void Engine::run_prefill_chunk(const std::vector<PrefillPiece>& pcs, float* logits_out) {
+  const int n = static_cast<int>(pcs.size());
   int T = 0;
-  for (int j = 0; j < n; ++j) T += static_cast<int>(offs[seq_index[j] + 1] - offs[seq_index[j]]);
+  for (const PrefillPiece& pc : pcs) T += pc.ntok;
   const size_t ints = 3 * static_cast<size_t>(T) + 8 * static_cast<size_t>(n) + 1;
   int32_t* m = stage_meta(ints);
   int32_t* in_tok = m;
@@ -433,24 +452,26 @@ void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t*
   int row = 0, items = 0;
   sum_ctx_sq_ = 0;
   for (int j = 0; j < n; ++j) {
-    const int64_t o = offs[seq_index[j]];
-    const int p = static_cast<int>(offs[seq_index[j] + 1] - o);
-    for (int t = 0; t < p; ++t) {
-      in_tok[row + t] = toks[o + t];
-      slot[row + t] = slots[j];
-      pos[row + t] = t;
+    const PrefillPiece& pc = pcs[j];
+    for (int t = 0; t < pc.ntok; ++t) {
+      in_tok[row + t] = pc.toks[t];
+      slot[row + t] = pc.slot;
+      pos[row + t] = pc.pos0 + t;
     }
-    seq_slot[j] = slots[j];
+    seq_slot[j] = pc.slot;
     seq_row0[j] = row;
-    seq_pos0[j] = 0;
-    seq_ntok[j] = p;
-    sum_ctx_sq_ += static_cast<double>(p) * (p + 1);
+    seq_pos0[j] = pc.pos0;
+    seq_ntok[j] = pc.ntok;
+    // attended keys summed over the piece's queries, x2 (the causal-attention flop count)
+    sum_ctx_sq_ += 2.0 * pc.ntok * pc.pos0 + static_cast<double>(pc.ntok) * (pc.ntok + 1);
     item_off[j] = items;
-    items += (p + tpi - 1) / tpi;
-    last_row[j] = row + p - 1;
-    gen_pos[j] = p;
-    gen_hist[j] = 0;
-    row += p;
+    items += (pc.ntok + tpi - 1) / tpi;
+    last_row[j] = row + pc.ntok - 1;
+    // A piece that does not end its sequence samples into the same history
+    // entry the final piece overwrites later.
+    gen_pos[j] = pc.pos0 + pc.ntok;
+    gen_hist[j] = pc.hist0;
+    row += pc.ntok;
   }
   item_off[n] = items;
   upload_meta(m, ints);
@@ -461,14 +482,23 @@ void Engine::run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t*
   m_gen_pos_ = m_last_row_ + n; m_gen_hist_ = m_gen_pos_ + n; m_gen_slot_ = m_seq_slot_;
   forward(T, true, n, items, 0, 0);
   if (logits_out) {
-    HIP_TRY(hipMemcpyAsync(logits_out + static_cast<size_t>(seq_index[0]) * cfg_.vocab, scratch_ + plan_.logits,
-                           static_cast<size_t>(n) * cfg_.vocab * 4, hipMemcpyDeviceToDevice, stream_));
+    // logits rows of the pieces that end a sequence, in runs of consecutive sequences
+    int j = 0;
+    while (j < n) {
+      if (pcs[j].seq < 0) { ++j; continue; }
+      int k = j + 1;
+      while (k < n && pcs[k].seq == pcs[k - 1].seq + 1) ++k;
+      HIP_TRY(hipMemcpyAsync(logits_out + static_cast<size_t>(pcs[j].seq) * cfg_.vocab,
+                             sp<float>(plan_.logits) + static_cast<size_t>(j) * cfg_.vocab,
+                             static_cast<size_t>(k - j) * cfg_.vocab * 4, hipMemcpyDeviceToDevice, stream_));
+      j = k;
+    }
   }
 }
 
-void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
-                     const int32_t* max_new, uint64_t seed, float temp, float* logits_out, int32_t* first_out) {
-  check_admission(n, ids, offs, toks, max_new, temp);
+std::vector<int32_t> Engine::admit_seqs(const std::vector<AdmitSeq>& a, const std::vector<const int32_t*>& restore,
+                                        float* logits_out) {
+  const int32_t n = static_cast<int32_t>(a.size());
   if (tables_pending_) {
     HIP_TRY(hipEventSynchronize(ev_tables_));
     tables_pending_ = false;
@@ -479,43 +509,80 @@ void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const i
     free_slots_.pop_back();
     Seq& q = slots_[s];
     q = Seq{};
-    q.id = ids[i];
-    q.prompt_len = static_cast<int32_t>(offs[i + 1] - offs[i]);
-    q.max_new = max_new[i];
-    q.seed = seed;
-    q.temp = temp;
+    q.id = a[i].id;
+    q.prompt_len = a[i].prompt_len;
+    q.max_new = a[i].max_new;
+    q.n_gen = a[i].n_gen0;
+    q.seed = a[i].seed;
+    q.temp = a[i].temp;
     q.live = true;
-    pool_.take(PagePool::pages_for(q.prompt_len + q.max_new - 1, kPageTokens), s, q.pages);
+    q.arrival = a[i].arrival;
+    if (kv_policy_ == RP_KV_ON_DEMAND) q.prompt.assign(a[i].toks, a[i].toks + a[i].prompt_len);
+    pool_.take(admit_pages(a[i].prompt_len, a[i].max_new, a[i].ntok), s, q.pages);
     int32_t* row = h_page_table_ + static_cast<size_t>(s) * plan_.max_pages;
     std::fill(row, row + plan_.max_pages, 0);
     std::copy(q.pages.begin(), q.pages.end(), row);
-    h_slot_seed_[s] = seed;
-    h_slot_id_[s] = static_cast<uint64_t>(ids[i]);
-    h_slot_temp_[s] = temp;
+    h_slot_seed_[s] = a[i].seed;
+    h_slot_id_[s] = static_cast<uint64_t>(a[i].id);
+    h_slot_temp_[s] = a[i].temp;
     id2slot_[q.id] = s;
     order_.push_back(s);
     new_slots[i] = s;
   }
   upload_slot_tables();
-  // Chunks of whole prompts with at most max_prefill_tokens tokens.
-  int32_t i = 0;
-  while (i < n) {
-    std::vector<int32_t> cs, ci;
-    int64_t tok = 0;
-    while (i < n) {
-      const int64_t p = offs[i + 1] - offs[i];
-      if (!cs.empty() && tok + p > lim_.max_prefill_tokens) break;
-      cs.push_back(new_slots[i]);
-      ci.push_back(i);
-      tok += p;
-      ++i;
+  // Tokens a resumed sequence generated before its preemption go back into its history row.
+  bool restored = false;
+  for (int32_t i = 0; i < n; ++i)
+    if (a[i].n_gen0 > 0 && restore[i]) {
+      HIP_TRY(hipMemcpyAsync(sp<int32_t>(plan_.hist) + static_cast<size_t>(new_slots[i]) * lim_.max_context,
+                             restore[i], static_cast<size_t>(a[i].n_gen0) * 4, hipMemcpyHostToDevice, stream_));
+      restored = true;
     }
-    run_prefill_chunk(cs, toks, offs, ci, logits_out);
+  if (restored) HIP_TRY(hipStreamSynchronize(stream_));
+  // Chunks of at most max_prefill_tokens tokens.  A sequence that fits is
+  // never split; a longer one is cut into pieces that continue at their
+  // position (the attention of a piece reads the earlier keys from its pages).
+  const int32_t budget = lim_.max_prefill_tokens;
+  std::vector<PrefillPiece> chunk;
+  int32_t tok = 0;
+  auto flush = [&]() {
+    if (!chunk.empty()) run_prefill_chunk(chunk, logits_out);
+    chunk.clear();
+    tok = 0;
+  };
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t len = a[i].ntok;
+    if (len <= budget) {
+      if (tok + len > budget) flush();
+      chunk.push_back({new_slots[i], a[i].toks, 0, len, a[i].n_gen0, i});
+      tok += len;
+      continue;
+    }
+    flush();
+    for (int32_t o = 0; o < len; o += budget) {
+      const int32_t take = std::min(budget, len - o);
+      chunk.push_back({new_slots[i], a[i].toks + o, o, take, a[i].n_gen0, o + take == len ? i : -1});
+      tok += take;
+      if (o + take < len) flush();
+    }
   }
+  flush();
   for (int32_t s : new_slots) {
-    slots_[s].n_gen = 1;
+    slots_[s].n_gen += 1;
     if (slots_[s].n_gen >= slots_[s].max_new) slots_[s].finished = true;
   }
+  return new_slots;
+}
+
+void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
+                     const int32_t* max_new, uint64_t seed, float temp, float* logits_out, int32_t* first_out) {
+  check_admission(n, ids, offs, toks, max_new, temp);
+  std::vector<AdmitSeq> a(n);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t p = static_cast<int32_t>(offs[i + 1] - offs[i]);
+    a[i] = AdmitSeq{ids[i], toks + offs[i], p, p, max_new[i], 0, seed, temp, arrival_next_++};
+  }
+  const std::vector<int32_t> new_slots = admit_seqs(a, std::vector<const int32_t*>(n, nullptr), logits_out);
   if (first_out) {
     HIP_TRY(hipStreamSynchronize(stream_));
     std::vector<int32_t> cur(lim_.max_seqs);
@@ -525,10 +592,14 @@ void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const i
 }
 
 int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* row_ids_out) {
+  if (forced && kv_policy_ == RP_KV_ON_DEMAND)
+    throw RpError(RP_ERR_INVALID_ARG, "teacher forcing needs the reserving KV policy");
+  std::vector<int32_t> resumed;
+  if (kv_policy_ == RP_KV_ON_DEMAND) resumed = schedule_pages();
   std::vector<int32_t> rows;
   rows.reserve(order_.size());
   for (int32_t s : order_)
-    if (!slots_[s].finished) rows.push_back(s);
+    if (!slots_[s].finished && std::find(resumed.begin(), resumed.end(), s) == resumed.end()) rows.push_back(s);
   const int B = static_cast<int>(rows.size());
   if (B == 0) return 0;
   if (forced) {
@@ -651,14 +722,133 @@ void Engine::abort(int32_t n, const int64_t* ids) {
   if (n < 0 || (n > 0 && !ids)) throw RpError(RP_ERR_INVALID_ARG, "abort: bad arguments");
   std::unordered_map<int64_t, int> seen;
   for (int32_t i = 0; i < n; ++i) {
-    if (!id2slot_.count(ids[i])) throw RpError(RP_ERR_UNKNOWN_ID, "abort: unknown sequence id");
+    if (!known_id(ids[i])) throw RpError(RP_ERR_UNKNOWN_ID, "abort: unknown sequence id");
     if (seen.count(ids[i])) throw RpError(RP_ERR_INVALID_ARG, "abort: duplicate id");
     seen[ids[i]] = 1;
   }
-  for (int32_t i = 0; i < n; ++i) release(id2slot_.at(ids[i]));
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = id2slot_.find(ids[i]);
+    if (it != id2slot_.end()) {
+      release(it->second);
+    } else {
+      waiting_.erase(std::find_if(waiting_.begin(), waiting_.end(), [&](const Waiting& w) { return w.id == ids[i]; }));
+    }
+  }
+}
+
+void Engine::set_kv_policy(int32_t policy) {
+  if (policy != RP_KV_RESERVE && policy != RP_KV_ON_DEMAND) throw RpError(RP_ERR_INVALID_ARG, "unknown KV policy");
+  if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "the KV policy changes only with no live sequences");
+  kv_policy_ = policy;
+}
+
+void Engine::kv_status(int64_t* free_pages, int32_t* running, int32_t* waiting, int64_t* preemptions,
+                       int64_t* recomputed_tokens) const {
+  if (free_pages) *free_pages = pool_.free_pages();
+  if (running) *running = static_cast<int32_t>(order_.size());
+  if (waiting) *waiting = static_cast<int32_t>(waiting_.size());
+  if (preemptions) *preemptions = n_preempt_;
+  if (recomputed_tokens) *recomputed_tokens = n_recompute_tok_;
+}
+
+void Engine::preempt(const std::vector<int32_t>& victims) {
+  if (victims.empty()) return;
+  HIP_TRY(hipStreamSynchronize(stream_));  // the history rows hold the last sampled tokens
+  for (int32_t s : victims) {
+    const Seq& q = slots_[s];
+    Waiting w{q.id, q.prompt_len, q.max_new, q.n_gen, q.seed, q.temp, q.arrival, q.prompt};
+    w.tokens.resize(static_cast<size_t>(q.prompt_len) + q.n_gen);
+    HIP_TRY(hipMemcpy(w.tokens.data() + q.prompt_len, sp<int32_t>(plan_.hist) + static_cast<size_t>(s) * lim_.max_context,
+                      static_cast<size_t>(q.n_gen) * 4, hipMemcpyDeviceToHost));
+    release(s);
+    waiting_.insert(std::upper_bound(waiting_.begin(), waiting_.end(), w.arrival,
+                                     [](int64_t a, const Waiting& x) { return a < x.arrival; }),
+                    std::move(w));
+    ++n_preempt_;
+  }
+}
+
+std::vector<int32_t> Engine::schedule_pages() {
+  // Pages the running rows need for the position each one writes next.
+  std::vector<int32_t> rows;
+  int64_t need = 0;
+  auto extra = [&](int32_t s) {
+    const Seq& q = slots_[s];
+    return std::max<int64_t>(0, PagePool::pages_for(q.prompt_len + q.n_gen, kPageTokens) -
+                                    static_cast<int64_t>(q.pages.size()));
+  };
+  for (int32_t s : order_)
+    if (!slots_[s].finished) {
+      rows.push_back(s);
+      need += extra(s);
+    }
+  // Resume preempted sequences, oldest arrival first, while the pool has
+  // room for them beyond what the running rows need this step.
+  std::vector<AdmitSeq> adm;
+  std::vector<const int32_t*> restore;
+  std::vector<Waiting> taken;
+  int64_t reserve = need;
+  size_t k = 0;
+  while (k < waiting_.size() && adm.size() < free_slots_.size()) {
+    const Waiting& w = waiting_[k];
+    const int64_t ntok = static_cast<int64_t>(w.prompt_len) + w.n_gen;
+    const int64_t pages = PagePool::pages_for(std::min<int64_t>(ntok + 1, w.prompt_len + w.max_new - 1), kPageTokens);
+    if (reserve + pages > pool_.free_pages()) break;
+    reserve += pages;
+    ++k;
+  }
+  if (k > 0) {
+    taken.assign(std::make_move_iterator(waiting_.begin()), std::make_move_iterator(waiting_.begin() + k));
+    waiting_.erase(waiting_.begin(), waiting_.begin() + k);
+    for (const Waiting& w : taken) {
+      const int32_t ntok = w.prompt_len + w.n_gen;
+      adm.push_back(AdmitSeq{w.id, w.tokens.data(), ntok, w.prompt_len, w.max_new, w.n_gen, w.seed, w.temp,
+                             w.arrival});
+      restore.push_back(w.tokens.data() + w.prompt_len);
+      n_recompute_tok_ += ntok;
+    }
+  }
+  std::vector<int32_t> resumed;
+  if (!adm.empty()) resumed = admit_seqs(adm, restore, nullptr);
+  // Preempt the latest arrivals until the remaining rows fit.
+  std::vector<int32_t> victims;
+  while (need > pool_.free_pages()) {
+    if (rows.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "KV pool held by finished sequences; free them first");
+    auto v = std::max_element(rows.begin(), rows.end(),
+                              [&](int32_t a, int32_t b) { return slots_[a].arrival < slots_[b].arrival; });
+    need -= extra(*v);
+    victims.push_back(*v);
+    rows.erase(v);
+  }
+  preempt(victims);
+  bool grew = false;
+  for (int32_t s : rows) {
+    const int64_t e = extra(s);
+    if (e == 0) continue;
+    if (!grew && tables_pending_) {
+      HIP_TRY(hipEventSynchronize(ev_tables_));
+      tables_pending_ = false;
+    }
+    Seq& q = slots_[s];
+    const size_t old = q.pages.size();
+    pool_.take(e, s, q.pages);
+    int32_t* row = h_page_table_ + static_cast<size_t>(s) * plan_.max_pages;
+    std::copy(q.pages.begin() + old, q.pages.end(), row + old);
+    grew = true;
+  }
+  if (grew) upload_slot_tables();
+  return resumed;
 }
 
 int32_t Engine::get_tokens(int64_t id, int32_t* out, int32_t cap) {
+  if (const Waiting* w = find_waiting(id)) {
+    const int32_t k = std::min(cap, w->n_gen);
+    if (k > 0) {
+      if (!out) throw RpError(RP_ERR_INVALID_ARG, "get_tokens: null output");
+      std::copy(w->tokens.begin() + w->prompt_len, w->tokens.begin() + w->prompt_len + k, out);
+    }
+    return w->n_gen;
+  }
   auto it = id2slot_.find(id);
   if (it == id2slot_.end()) throw RpError(RP_ERR_UNKNOWN_ID, "get_tokens: unknown sequence id");
   const Seq& q = slots_[it->second];
@@ -681,8 +871,8 @@ void Engine::validate_seqs(int32_t n, const int64_t* ids, const int32_t* toks, c
   for (int32_t i = 0; i < n; ++i) {
     const int64_t p = offs[i + 1] - offs[i];
     if (p < 1 || max_new[i] < 1) throw RpError(RP_ERR_INVALID_ARG, "prompts and max_new_tokens must be >= 1");
-    if (p > lim_.max_prefill_tokens || p + max_new[i] - 1 > lim_.max_context)
-      throw RpError(RP_ERR_CAPACITY, "a sequence exceeds max_prefill_tokens or max_context");
+    if (p + max_new[i] - 1 > lim_.max_context)
+      throw RpError(RP_ERR_CAPACITY, "a sequence exceeds max_context");
     if (PagePool::pages_for(p + max_new[i] - 1, kPageTokens) > pool_.capacity())
       throw RpError(RP_ERR_OUT_OF_PAGES, "a sequence needs more pages than the pool holds");
     if (seen.count(ids[i])) throw RpError(RP_ERR_DUPLICATE_ID, "duplicate sequence id");
@@ -715,10 +905,16 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
   std::vector<std::pair<size_t, int32_t>> left_ev;     // (event index, member position) per departure
   std::vector<std::array<int64_t, 3>> pending_copies;  // dev offset, host offset, length
   size_t resp_cursor = 0;
-  std::unordered_map<int32_t, int32_t> slot_member;    // slot -> position in members
+  std::unordered_map<int64_t, int32_t> id_member;      // sequence id -> position in members
   pool_.reset_peak();
   int32_t steps = 0;
   int64_t prompt_tokens = 0, gen_tokens = 0;
+  const int64_t preempt0 = n_preempt_, recompute0 = n_recompute_tok_;
+  // On demand, fresh sequences are admitted only while no preempted one waits
+  // and a watermark of 1% of the pool stays free (none for a race round,
+  // which starts everything at once).
+  const bool on_demand = kv_policy_ == RP_KV_ON_DEMAND;
+  const int64_t watermark = on_demand && !race ? std::max<int64_t>(1, pool_.capacity() / 100) : 0;
 
   // Race bookkeeping: finished members per prompt in completion order, and
   // whether each prompt has been decided (accepted, or lost the race).
@@ -741,31 +937,32 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     resp_cursor = 0;
   };
   auto admit = [&]() {
+    if (!waiting_.empty()) return;
     std::vector<int64_t> b_ids, b_offs{0};
     std::vector<int32_t> b_toks, b_new, b_mem;
     int64_t pages = 0;
     while (next < members.size() && b_ids.size() < free_slots_.size()) {
       const int32_t i = members[next];
-      const int64_t need = PagePool::pages_for(a.offs[i + 1] - a.offs[i] + a.max_new[i] - 1, kPageTokens);
-      if (!pool_.can_take(pages + need)) break;
+      const int64_t p = a.offs[i + 1] - a.offs[i];
+      const int64_t need = admit_pages(p, a.max_new[i], p);
+      if (!pool_.can_take(pages + need + watermark)) break;
       pages += need;
       b_ids.push_back(a.ids[i]);
       b_toks.insert(b_toks.end(), a.toks + a.offs[i], a.toks + a.offs[i + 1]);
       b_offs.push_back(static_cast<int64_t>(b_toks.size()));
       b_new.push_back(a.max_new[i]);
       b_mem.push_back(static_cast<int32_t>(next));
-      prompt_tokens += a.offs[i + 1] - a.offs[i];
+      prompt_tokens += p;
       ++next;
     }
     if (b_ids.empty()) return;
-    const size_t before = order_.size();
     prefill(static_cast<int32_t>(b_ids.size()), b_ids.data(), b_toks.data(), b_offs.data(), b_new.data(), a.seed,
             a.temp, nullptr, nullptr);
-    for (size_t k = 0; k < b_mem.size(); ++k) slot_member[order_[before + k]] = b_mem[k];
+    for (size_t k = 0; k < b_mem.size(); ++k) id_member[b_ids[k]] = b_mem[k];
   };
   // Copies a departing sequence's tokens out, then frees its slot and pages.
   auto retire = [&](int32_t s) {
-    const int32_t k = slot_member.at(s);
+    const int32_t k = id_member.at(slots_[s].id);
     const int32_t i = members[k];
     const int64_t len = slots_[s].n_gen;
     if (resp_cursor + len > resp_cap) flush();
@@ -776,8 +973,18 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     if (gen_out) gen_out[i] = static_cast<int32_t>(len);
     left_ev.push_back({n_ev, k});
     gen_tokens += len;
-    slot_member.erase(s);
+    id_member.erase(slots_[s].id);
     release(s);
+  };
+  // The same for a preempted member: its tokens are on the host already.
+  auto retire_waiting = [&](const Waiting& w) {
+    const int32_t k = id_member.at(w.id);
+    const int32_t i = members[k];
+    std::copy(w.tokens.begin() + w.prompt_len, w.tokens.end(), resp_out + a.resp_off[i]);
+    if (gen_out) gen_out[i] = w.n_gen;
+    left_ev.push_back({n_ev, k});
+    gen_tokens += w.n_gen;
+    id_member.erase(w.id);
   };
   auto collect = [&]() {
     std::vector<int32_t> leaving;
@@ -785,15 +992,20 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     bool stop = false;
     if (race) {
       // Completions of this step, in member order (responses of a prompt by index).
-      std::vector<int32_t> fresh;
+      std::vector<std::pair<int32_t, int32_t>> fin;  // (member, prompt)
       for (int32_t s : order_)
         if (slots_[s].finished) {
-          const int32_t k = slot_member.at(s);
-          const int32_t p = race->prompt[k];
-          if (decided[p]) continue;
-          done[p].push_back(k);
-          if (static_cast<int32_t>(done[p].size()) == race->R0) fresh.push_back(p);
+          const int32_t k = id_member.at(slots_[s].id);
+          fin.push_back({k, race->prompt[k]});
         }
+      std::sort(fin.begin(), fin.end());
+      std::vector<int32_t> fresh;
+      for (auto& f : fin) {
+        const int32_t p = f.second;
+        if (decided[p]) continue;
+        done[p].push_back(f.first);
+        if (static_cast<int32_t>(done[p].size()) == race->R0) fresh.push_back(p);
+      }
       std::sort(fresh.begin(), fresh.end());
       abort_prompt.assign(race->n_prompts, 0);
       for (int32_t p : fresh) {
@@ -807,12 +1019,23 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
       }
       stop = n_acc >= race->keep;
     }
-    for (int32_t s : order_) {
-      const bool fin = slots_[s].finished;
-      if (fin || stop || (race && abort_prompt[race->prompt[slot_member.at(s)]])) leaving.push_back(s);
-    }
-    if (leaving.empty()) return;
+    auto goes = [&](int64_t id) { return stop || (race && abort_prompt[race->prompt[id_member.at(id)]]); };
+    for (int32_t s : order_)
+      if (slots_[s].finished || goes(slots_[s].id)) leaving.push_back(s);
+    bool any = !leaving.empty();
     for (int32_t s : leaving) retire(s);
+    if (race) {
+      for (size_t w = 0; w < waiting_.size();) {
+        if (id_member.count(waiting_[w].id) && goes(waiting_[w].id)) {
+          retire_waiting(waiting_[w]);
+          waiting_.erase(waiting_.begin() + static_cast<std::ptrdiff_t>(w));
+          any = true;
+        } else {
+          ++w;
+        }
+      }
+    }
+    if (!any) return;
     HIP_TRY(hipEventRecord(event_at(n_ev), stream_));
     ++n_ev;
   };
@@ -828,8 +1051,8 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
       admit();
       collect();
     }
-    if (order_.empty() && next >= members.size()) break;
-    if (order_.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "rollout: a sequence cannot be admitted");
+    if (order_.empty() && waiting_.empty() && next >= members.size()) break;
+    if (order_.empty() && waiting_.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "rollout: a sequence cannot be admitted");
     decode_step(nullptr, nullptr, nullptr);
     ++steps;
     collect();
@@ -849,6 +1072,8 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
   st->prompt_tokens = prompt_tokens;
   st->generated_tokens = gen_tokens;
   st->peak_pages = pool_.peak_used();
+  st->preemptions = n_preempt_ - preempt0;
+  st->recomputed_tokens = n_recompute_tok_ - recompute0;
   HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_end));
   st->makespan_ms = ms;
   HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_pre));
@@ -867,7 +1092,7 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
 int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
                         const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
                         int32_t* resp_out, rp_round_stats* stats, int32_t max_stats) {
-  if (!order_.empty()) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
+  if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
   if (n < 1 || !ids || !toks || !offs || !max_new || !resp_out)
     throw RpError(RP_ERR_INVALID_ARG, "rollout: null array or n < 1");
   std::vector<int64_t> resp_off;
@@ -888,17 +1113,18 @@ int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, cons
 
 int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const int64_t* ids, const int32_t* ptoks,
                                      const int64_t* poffs, const int32_t* max_new, uint64_t seed, float temp,
-                                     int32_t P0, int32_t R0, float eta, int32_t* resp_out, int32_t* gen_out,
+                                     int32_t P0, int32_t R0, float eta_p, float eta_r, int32_t* resp_out,
+                                     int32_t* gen_out,
                                      int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
                                      int32_t max_stats) {
-  if (!order_.empty()) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
+  if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
   if (n_prompts < 1 || r_spec < 1 || !ids || !ptoks || !poffs || !max_new || !resp_out || !gen_out ||
       !accept_round_out || !kept_out)
     throw RpError(RP_ERR_INVALID_ARG, "tail-batched rollout: null array or n_prompts < 1");
-  if (P0 < 1 || R0 < 1 || !(eta >= 1.f) || std::isinf(eta))
-    throw RpError(RP_ERR_INVALID_ARG, "tail-batched rollout needs P0 >= 1, R0 >= 1 and a finite eta >= 1");
-  if (r_spec != static_cast<int32_t>(std::ceil(static_cast<double>(eta) * R0 - 1e-9)))
-    throw RpError(RP_ERR_INVALID_ARG, "r_spec must equal ceil(eta * R0)");
+  if (P0 < 1 || R0 < 1 || !(eta_p >= 1.f) || !(eta_r >= 1.f) || std::isinf(eta_p) || std::isinf(eta_r) ||
+      static_cast<double>(eta_p) * P0 > 1e9)
+    throw RpError(RP_ERR_INVALID_ARG, "tail-batched rollout needs P0 >= 1, R0 >= 1 and finite eta_p, eta_r >= 1");
+  if (r_spec != spec_count(eta_r, R0)) throw RpError(RP_ERR_INVALID_ARG, "r_spec must equal ceil(eta_r * R0)");
   if (static_cast<int64_t>(n_prompts) * r_spec > (int64_t{1} << 30))
     throw RpError(RP_ERR_INVALID_ARG, "too many responses");
   if (poffs[0] != 0) throw RpError(RP_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
@@ -920,13 +1146,13 @@ int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const in
 
   // A short round starts every launched response at once: check that each
   // one fits before anything runs.
-  const int32_t p_spec = static_cast<int32_t>(std::ceil(static_cast<double>(eta) * P0 - 1e-9));
+  const int32_t p_spec = spec_count(eta_p, P0);
   for (int32_t p0 = 0; p0 < n_prompts; p0 += p_spec) {
     int64_t pages = 0, seqs = 0;
     for (int32_t p = p0; p < std::min(n_prompts, p0 + p_spec); ++p)
       for (int32_t r = 0; r < r_spec; ++r) {
         const size_t i = static_cast<size_t>(p) * r_spec + r;
-        pages += PagePool::pages_for(offs[i + 1] - offs[i] + max_new[i] - 1, kPageTokens);
+        pages += admit_pages(offs[i + 1] - offs[i], max_new[i], offs[i + 1] - offs[i]);
         ++seqs;
       }
     if (seqs > lim_.max_seqs || pages > pool_.capacity())
@@ -958,7 +1184,7 @@ int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const in
         for (int32_t r = 0; r < R0; ++r) kept_out[p * r_spec + r] = 1;
       }
     } else {
-      // Short round: race to completion among the next ceil(eta * P0) fresh prompts.
+      // Short round: race to completion among the next ceil(eta_p * P0) fresh prompts.
       st.kind = 0;
       for (int32_t j = 0; j < p_spec && next_fresh < n_prompts; ++j) launched.push_back(next_fresh++);
       Race race;

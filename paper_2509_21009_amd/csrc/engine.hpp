@@ -45,7 +45,39 @@ struct Seq {
   float temp = 0.f;
   bool live = false;
   bool finished = false;
+  int64_t arrival = 0;   // admission order of the sequence's first prefill
   std::vector<int32_t> pages;
+  std::vector<int32_t> prompt;  // kept under on-demand pages, for a recompute after preemption
+};
+
+// A sequence preempted under KV pressure: its pages and slot are gone, its
+// tokens wait on the host until it is recomputed.
+struct Waiting {
+  int64_t id;
+  int32_t prompt_len, max_new, n_gen;
+  uint64_t seed;
+  float temp;
+  int64_t arrival;
+  std::vector<int32_t> tokens;  // prompt followed by the n_gen generated tokens
+};
+
+// One sequence to (re)admit: prefill `ntok` tokens at positions 0..ntok-1 and
+// sample the token at position ntok into history entry n_gen0.
+struct AdmitSeq {
+  int64_t id;
+  const int32_t* toks;
+  int32_t ntok, prompt_len, max_new, n_gen0;
+  uint64_t seed;
+  float temp;
+  int64_t arrival;
+};
+
+// A contiguous run of one sequence's tokens inside a prefill chunk.
+struct PrefillPiece {
+  int32_t slot;
+  const int32_t* toks;
+  int32_t pos0, ntok, hist0;
+  int32_t seq;  // index of the sequence in its admit call; -1 unless the piece ends it
 };
 
 // Per-sequence inputs of one rollout call (prompt CSR per sequence).
@@ -86,16 +118,20 @@ class Engine {
                   int32_t* resp_out, rp_round_stats* stats, int32_t max_stats);
   int32_t rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const int64_t* ids, const int32_t* ptoks,
                                const int64_t* poffs, const int32_t* max_new, uint64_t seed, float temp,
-                               int32_t P0, int32_t R0, float eta, int32_t* resp_out, int32_t* gen_out,
+                               int32_t P0, int32_t R0, float eta_p, float eta_r, int32_t* resp_out,
+                               int32_t* gen_out,
                                int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
                                int32_t max_stats);
 
   void profile_enable(uint32_t mask);
   int32_t profile_read(rp_kernel_stats* out, int32_t cap);
+  void set_kv_policy(int32_t policy);
+  void kv_status(int64_t* free_pages, int32_t* running, int32_t* waiting, int64_t* preemptions,
+                 int64_t* recomputed_tokens) const;
 
   bool broken() const { return broken_; }
   void mark_broken() { broken_ = true; }
-  int32_t live_count() const { return static_cast<int32_t>(order_.size()); }
+  int32_t live_count() const { return static_cast<int32_t>(order_.size() + waiting_.size()); }
 
  private:
   struct Staging {
@@ -110,8 +146,19 @@ class Engine {
   void upload_slot_tables();
   void check_admission(int32_t n, const int64_t* ids, const int64_t* offs, const int32_t* toks,
                        const int32_t* max_new, float temp) const;
-  void run_prefill_chunk(const std::vector<int32_t>& slots, const int32_t* toks, const int64_t* offs,
-                         const std::vector<int32_t>& seq_index, float* logits_out);
+  // Pages a sequence takes at admission: its whole length when reserving,
+  // else the tokens to prefill (on demand).
+  int64_t admit_pages(int64_t prompt_len, int64_t max_new, int64_t ntok) const;
+  std::vector<int32_t> admit_seqs(const std::vector<AdmitSeq>& a, const std::vector<const int32_t*>& restore,
+                                  float* logits_out);
+  void run_prefill_chunk(const std::vector<PrefillPiece>& pcs, float* logits_out);
+  // On-demand pages: resume waiting sequences that fit, then give every
+  // running row a page for its next position, preempting the latest arrivals
+  // when the pool runs dry.  Returns the slots resumed (they advanced already).
+  std::vector<int32_t> schedule_pages();
+  void preempt(const std::vector<int32_t>& victims);
+  bool known_id(int64_t id) const;
+  Waiting* find_waiting(int64_t id);
   void release(int32_t slot);
   void validate_seqs(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
                      const int32_t* max_new, float temp, std::vector<int64_t>& resp_off) const;
@@ -140,6 +187,10 @@ class Engine {
   std::vector<Seq> slots_;
   std::vector<int32_t> free_slots_;
   std::vector<int32_t> order_;  // live slots in admission order
+  std::vector<Waiting> waiting_;  // preempted sequences, by arrival
+  int32_t kv_policy_ = RP_KV_RESERVE;
+  int64_t arrival_next_ = 0;
+  int64_t n_preempt_ = 0, n_recompute_tok_ = 0;
   std::unordered_map<int64_t, int32_t> id2slot_;
   // pinned host mirrors
   int32_t* h_page_table_ = nullptr;

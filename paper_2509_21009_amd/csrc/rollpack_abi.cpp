@@ -146,20 +146,22 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
 rp_status rp_rollout_tail_batched(rp_engine* eng, int32_t n_prompts, int32_t r_spec, const int64_t* seq_ids,
                                   const int32_t* prompt_tokens, const int64_t* prompt_offsets,
                                   const int32_t* max_new_tokens, uint64_t seed, float temperature, int32_t P0,
-                                  int32_t R0, float eta, int32_t* resp_tokens_out, int32_t* resp_len_out,
+                                  int32_t R0, float eta_p, float eta_r, int32_t* resp_tokens_out,
+                                  int32_t* resp_len_out,
                                   int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats_out,
                                   int32_t max_stats, int32_t* n_rounds_out) {
   return engine_call(eng, [&](rollpack::Engine* e) {
     if (max_stats < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "max_stats must be >= 0");
     const int32_t r = e->rollout_tail_batched(n_prompts, r_spec, seq_ids, prompt_tokens, prompt_offsets,
-                                              max_new_tokens, seed, temperature, P0, R0, eta, resp_tokens_out,
+                                              max_new_tokens, seed, temperature, P0, R0, eta_p, eta_r,
+                                              resp_tokens_out,
                                               resp_len_out, accept_round_out, kept_out, stats_out, max_stats);
     if (n_rounds_out) *n_rounds_out = r;
   });
 }
 
 rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens, int32_t P0, int32_t R0,
-                                float eta, int32_t max_rounds, int32_t cap_launch, int32_t* round_kind_out,
+                                float eta_p, float eta_r, int32_t max_rounds, int32_t cap_launch, int32_t* round_kind_out,
                                 int32_t* round_time_out, int32_t* launch_off_out, int32_t* launch_prompt_out,
                                 int32_t* run_steps_out, int32_t* accept_round_out, int32_t* kept_out,
                                 int32_t* n_rounds_out) {
@@ -169,7 +171,7 @@ rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t
       throw rollpack::RpError(RP_ERR_INVALID_ARG, "tail batching: bad arguments");
     for (int64_t i = 0; i < static_cast<int64_t>(n_prompts) * r_spec; ++i)
       if (lens[i] < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "tail batching: negative length");
-    const rollpack::TailBatchPlan plan = rollpack::plan_tail_batching(n_prompts, r_spec, lens, P0, R0, eta);
+    const rollpack::TailBatchPlan plan = rollpack::plan_tail_batching(n_prompts, r_spec, lens, P0, R0, eta_p, eta_r);
     const int32_t nr = static_cast<int32_t>(plan.rounds.size());
     size_t launches = 0;
     for (const auto& r : plan.rounds) launches += r.launched.size();
@@ -193,6 +195,17 @@ rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t
     for (int32_t p = 0; p < n_prompts; ++p) accept_round_out[p] = plan.accept_round[p];
     for (size_t i = 0; i < plan.kept.size(); ++i) kept_out[i] = plan.kept[i];
     *n_rounds_out = nr;
+  });
+}
+
+rp_status rp_set_kv_policy(rp_engine* eng, int32_t policy) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->set_kv_policy(policy); });
+}
+
+rp_status rp_kv_status(rp_engine* eng, int64_t* free_pages, int32_t* running, int32_t* waiting, int64_t* preemptions,
+                       int64_t* recomputed_tokens) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    e->kv_status(free_pages, running, waiting, preemptions, recomputed_tokens);
   });
 }
 

@@ -23,13 +23,18 @@ std::vector<int32_t> shortest_k(const int32_t* row, int32_t r_spec, int32_t k) {
 
 }  // namespace
 
+int32_t spec_count(double eta, int32_t k) {
+  const double x = eta * k;
+  return static_cast<int32_t>(std::ceil(x - 1e-6 * x));
+}
+
 TailBatchPlan plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens,
-                                 int32_t P0, int32_t R0, double eta) {
-  if (n_prompts < 0 || P0 < 1 || R0 < 1 || !(eta >= 1.0))
-    throw std::invalid_argument("tail batching needs n >= 0, P0 >= 1, R0 >= 1, eta >= 1");
-  const int32_t want_r = static_cast<int32_t>(std::ceil(eta * R0 - 1e-9));
-  if (r_spec != want_r) throw std::invalid_argument("r_spec must equal ceil(eta * R0)");
-  const int32_t p_spec = static_cast<int32_t>(std::ceil(eta * P0 - 1e-9));
+                                 int32_t P0, int32_t R0, double eta_p, double eta_r) {
+  if (n_prompts < 0 || P0 < 1 || R0 < 1 || !(eta_p >= 1.0) || !(eta_r >= 1.0) || std::isinf(eta_p) ||
+      std::isinf(eta_r) || eta_p * P0 > 1e9 || eta_r * R0 > 1e9)
+    throw std::invalid_argument("tail batching needs n >= 0, P0 >= 1, R0 >= 1 and finite eta_p, eta_r >= 1");
+  if (r_spec != spec_count(eta_r, R0)) throw std::invalid_argument("r_spec must equal ceil(eta_r * R0)");
+  const int32_t p_spec = spec_count(eta_p, P0);
 
   TailBatchPlan plan;
   plan.accept_round.assign(n_prompts, -1);
@@ -61,7 +66,7 @@ TailBatchPlan plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_
       }
       rnd.accepted = rnd.launched;
     } else {
-      // Short round: race to completion among ceil(eta*P0) fresh prompts.
+      // Short round: race to completion among ceil(eta_p*P0) fresh prompts.
       rnd.kind = 0;
       for (int32_t i = 0; i < p_spec && next_fresh < n_prompts; ++i) rnd.launched.push_back(next_fresh++);
       const size_t n = rnd.launched.size();

@@ -1,9 +1,10 @@
 // Tail-batching round planner (paper section 3), host only.
 //
 // Each rollout step needs P0 prompts with R0 responses each.  A short round
-// over-provisions: it launches ceil(eta*P0) prompts with ceil(eta*R0)
-// responses each and keeps the first P0 prompts to complete, each with its
-// first R0 completed responses ("race to completion").  Prompts aborted in a
+// over-provisions: it launches ceil(eta_p*P0) prompts with ceil(eta_r*R0)
+// responses each (section 6.3 varies the two factors separately) and keeps
+// the first P0 prompts to complete, each with its first R0 completed
+// responses ("race to completion").  Prompts aborted in a
 // short round join a FIFO long-prompt queue; when the queue holds P0 prompts
 // they run as a long round with speculation disabled, so no prompt is ever
 // dropped.  With forced response lengths, "first to complete" is decided by
@@ -11,8 +12,11 @@
 //
 // Readings where the paper is silent: ties go to the lower index; the round
 // ends when its P0-th prompt completes; a short round with fewer than
-// ceil(eta*P0) fresh prompts launches what is left and keeps min(P0, n);
+// ceil(eta_p*P0) fresh prompts launches what is left and keeps min(P0, n);
 // when no fresh prompt is left, queued prompts are flushed in long rounds.
+// A product eta*P0 within one part in 10^6 of an integer counts as that
+// integer, so that factors such as 1.1 given in single precision round as
+// their decimal value does.
 #pragma once
 
 #include <cstdint>
@@ -35,9 +39,12 @@ struct TailBatchPlan {
   std::vector<uint8_t> kept;          // [n_prompts * r_spec]
 };
 
+// ceil(eta * k) with the tolerance above.
+int32_t spec_count(double eta, int32_t k);
+
 // lens: [n_prompts * r_spec] response lengths (>= 0).  Requires P0, R0 >= 1,
-// eta >= 1 and r_spec == ceil(eta * R0).
+// eta_p, eta_r >= 1 and r_spec == spec_count(eta_r, R0).
 TailBatchPlan plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens,
-                                 int32_t P0, int32_t R0, double eta);
+                                 int32_t P0, int32_t R0, double eta_p, double eta_r);
 
 }  // namespace rollpack

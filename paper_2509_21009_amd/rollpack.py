@@ -50,7 +50,8 @@ class RpRoundStats(ctypes.Structure):
                 ("kind", ctypes.c_int32), ("prompt_tokens", ctypes.c_int64),
                 ("generated_tokens", ctypes.c_int64), ("peak_pages", ctypes.c_int64),
                 ("makespan_ms", ctypes.c_double), ("prefill_ms", ctypes.c_double),
-                ("decode_ms", ctypes.c_double), ("slot_idle", ctypes.c_double), ("idle_slot_s", ctypes.c_double)]
+                ("decode_ms", ctypes.c_double), ("slot_idle", ctypes.c_double), ("idle_slot_s", ctypes.c_double),
+                ("preemptions", ctypes.c_int64), ("recomputed_tokens", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -100,11 +101,13 @@ SIGNATURES = {
                                            ctypes.c_int32, _I32P]),
     "rp_rollout_tail_batched": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P,
                                                ctypes.c_uint64, ctypes.c_float, ctypes.c_int32, ctypes.c_int32,
-                                               ctypes.c_float, _I32P, _I32P, _I32P, _I32P,
+                                               ctypes.c_float, ctypes.c_float, _I32P, _I32P, _I32P, _I32P,
                                                ctypes.POINTER(RpRoundStats), ctypes.c_int32, _I32P]),
     "rp_plan_tail_batching": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_int32, ctypes.c_int32,
-                                             ctypes.c_float, ctypes.c_int32, ctypes.c_int32, _I32P, _I32P, _I32P,
+                                             ctypes.c_float, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, _I32P, _I32P, _I32P,
                                              _I32P, _I32P, _I32P, _I32P, _I32P]),
+    "rp_set_kv_policy": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "rp_kv_status": (ctypes.c_int, [_P, _I64P, _I32P, _I32P, _I64P, _I64P]),
     "rp_profile_enable": (ctypes.c_int, [_P, ctypes.c_uint32]),
     "rp_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(RpKernelStats), ctypes.c_int32, _I32P]),
     "rp_last_error": (ctypes.c_char_p, []),
@@ -229,8 +232,10 @@ def rp_rollout_generate(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_ne
 
 
 def rp_rollout_tail_batched(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed: int,
-                            temperature: float, P0: int, R0: int, eta: float, max_stats: int = 0):
-    """seq_ids, max_new_tokens: [n_prompts, r_spec]; prompt CSR over prompts.
+                            temperature: float, P0: int, R0: int, eta: float, eta_r: Optional[float] = None,
+                            max_stats: int = 0):
+    """seq_ids, max_new_tokens: [n_prompts, r_spec]; prompt CSR over prompts.  eta is the prompt
+    speculation factor and, unless eta_r is given, the response factor too.
 
     Returns (resp_tokens, resp_len [n, r_spec], accept_round [n], kept [n, r_spec] bool, round stats)."""
     ids = np.ascontiguousarray(seq_ids, np.int64)
@@ -249,13 +254,15 @@ def rp_rollout_tail_batched(eng: int, seq_ids, prompt_tokens, prompt_offsets, ma
     P = lambda a: a.ctypes.data_as(_I32P)  # noqa: E731
     _check(load_library().rp_rollout_tail_batched(eng, n, r_spec, ids.ctypes.data_as(_I64P), toks_p, offs_p, P(mn),
                                                   ctypes.c_uint64(seed), ctypes.c_float(temperature), P0, R0,
-                                                  ctypes.c_float(eta), P(resp), P(glen), P(acc), P(kept), stats,
+                                                  ctypes.c_float(eta), ctypes.c_float(eta if eta_r is None else eta_r),
+                                                  P(resp), P(glen), P(acc), P(kept), stats,
                                                   max_stats, ctypes.byref(nr)))
     return resp, glen, acc, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
 
 
-def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float):
-    """lens: int array [n_prompts, r_spec].  Returns a list of round dicts and per-prompt arrays."""
+def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float, eta_r: Optional[float] = None):
+    """lens: int array [n_prompts, r_spec].  Returns a list of round dicts and per-prompt arrays.
+    eta is the prompt speculation factor and, unless eta_r is given, the response factor too."""
     lens = np.ascontiguousarray(lens, np.int32)
     n, r_spec = lens.shape
     max_rounds = 2 * n + 2
@@ -269,7 +276,8 @@ def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float):
     kept = np.zeros(max(n * r_spec, 1), np.int32)
     nr = ctypes.c_int32()
     P = lambda a: a.ctypes.data_as(_I32P)  # noqa: E731
-    _check(load_library().rp_plan_tail_batching(n, r_spec, P(lens), P0, R0, ctypes.c_float(eta), max_rounds, cap,
+    _check(load_library().rp_plan_tail_batching(n, r_spec, P(lens), P0, R0, ctypes.c_float(eta),
+                                                ctypes.c_float(eta if eta_r is None else eta_r), max_rounds, cap,
                                                 P(kind), P(rtime), P(loff), P(lp), P(run), P(acc), P(kept),
                                                 ctypes.byref(nr)))
     rounds = []
@@ -279,6 +287,22 @@ def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float):
         rounds.append({"kind": "long" if kind[k] else "short", "time": int(rtime[k]), "launched": launched,
                        "run": {(p, r): int(steps[i, r]) for i, p in enumerate(launched) for r in range(r_spec)}})
     return rounds, acc[:n].copy(), kept[:n * r_spec].reshape(n, r_spec).astype(bool)
+
+
+KV_RESERVE, KV_ON_DEMAND = 0, 1
+
+
+def rp_set_kv_policy(eng: int, policy: int) -> None:
+    _check(load_library().rp_set_kv_policy(eng, policy))
+
+
+def rp_kv_status(eng: int) -> dict:
+    f, p, rt = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    r, w = ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().rp_kv_status(eng, ctypes.byref(f), ctypes.byref(r), ctypes.byref(w), ctypes.byref(p),
+                                       ctypes.byref(rt)))
+    return {"free_pages": f.value, "running": r.value, "waiting": w.value, "preemptions": p.value,
+            "recomputed_tokens": rt.value}
 
 
 def rp_profile_enable(eng: int, classes) -> None:
@@ -381,6 +405,12 @@ class Engine:
     def get_tokens(self, seq_id: int, cap: int):
         return rp_get_tokens(self.handle, seq_id, cap)
 
+    def set_kv_policy(self, policy: int):
+        rp_set_kv_policy(self.handle, policy)
+
+    def kv_status(self) -> dict:
+        return rp_kv_status(self.handle)
+
     def profile(self, classes):
         rp_profile_enable(self.handle, classes)
 
@@ -393,9 +423,9 @@ class Engine:
 
 
     def rollout_tail_batched(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
-                             P0: int, R0: int, eta: float):
+                             P0: int, R0: int, eta: float, eta_r: Optional[float] = None):
         return rp_rollout_tail_batched(self.handle, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
-                                       temperature, P0, R0, eta)
+                                       temperature, P0, R0, eta, eta_r)
 
 
 def weights_for_engine(w: dict) -> dict:

@@ -83,7 +83,7 @@ static void test_plan_invariants() {
     const int r_spec = static_cast<int>(std::ceil(eta * R0 - 1e-9));
     std::vector<int32_t> lens(static_cast<size_t>(n) * r_spec);
     for (auto& L : lens) L = 1 + rng() % 500;
-    auto plan = rollpack::plan_tail_batching(n, r_spec, lens.data(), P0, R0, eta);
+    auto plan = rollpack::plan_tail_batching(n, r_spec, lens.data(), P0, R0, eta, eta);
     std::vector<int> accepted(n, 0);
     for (const auto& r : plan.rounds) {
       for (int32_t p : r.accepted) accepted[p]++;

@@ -97,16 +97,16 @@ def _lens(seed, n, r_spec):
     return np.clip(np.rint(300 * np.exp(0.9 * rng.standard_normal((n, r_spec)))), 1, 8000).astype(np.int32)
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(16))
 def test_tail_batching_plan_matches_oracle(lib, seed):
     rng = np.random.default_rng(seed)
-    P0, R0 = int(rng.integers(1, 9)), int(rng.integers(1, 9))
-    eta = float(rng.choice([1.0, 1.25, 1.5]))
-    r_spec = math.ceil(eta * R0)
+    P0, R0 = int(rng.integers(1, 11)), int(rng.integers(1, 11))
+    eta_p, eta_r = (float(rng.choice([1.0, 1.1, 1.25, 1.5])) for _ in range(2))
+    r_spec = osch.spec_count(eta_r, R0)
     n = int(rng.integers(0, 60))
     lens = _lens(seed, n, r_spec)
-    ours, acc, kept = rp.rp_plan_tail_batching(lens.reshape(n, r_spec), P0, R0, eta)
-    ref = osch.plan_tail_batching(lens.tolist(), P0, R0, eta)
+    ours, acc, kept = rp.rp_plan_tail_batching(lens.reshape(n, r_spec), P0, R0, eta_p, eta_r)
+    ref = osch.plan_tail_batching(lens.tolist(), P0, R0, eta_p, eta_r)
     assert len(ours) == len(ref)
     for a, b in zip(ours, ref):
         assert a["kind"] == b["kind"] and a["time"] == b["time"]
@@ -160,6 +160,8 @@ def test_rl_batch_lengths_are_prompt_correlated():
     assert len(set(a.seq_ids.reshape(-1).tolist())) == 2000
     same = make_rl_batch(s, 50, 4, sigma_p=0.6, sigma_r=0.0, **kw)      # no per-response spread
     assert (same.max_new == same.max_new[:, :1]).all()
+    wider = make_rl_batch(s, 200, 12, sigma_p=0.6, sigma_r=0.53, **kw)  # more responses, same first ten
+    assert np.array_equal(wider.max_new[:, :10], a.max_new) and np.array_equal(wider.prompt_tokens, a.prompt_tokens)
     # log-length variance splits into a between-prompt part (~sigma_p^2) and a within part (~sigma_r^2)
     lg = np.log(make_rl_batch(s, 2000, 10, sigma_p=0.6, sigma_r=0.53, p_lo=64, p_hi=512, median=512, lo=1,
                               hi=10**7, seed=8).max_new)

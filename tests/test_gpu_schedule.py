@@ -47,26 +47,29 @@ def _expected_lengths(plan_rounds, n, r_spec):
     return last
 
 
-CASES = [  # n_prompts, P0, R0, eta, seed
-    (12, 4, 2, 1.5, 11),
-    (10, 3, 3, 1.25, 12),
-    (7, 2, 2, 1.0, 13),
+CASES = [  # n_prompts, P0, R0, eta_p, eta_r, seed
+    (12, 4, 2, 1.5, 1.5, 11),
+    (10, 3, 3, 1.25, 1.25, 12),
+    (7, 2, 2, 1.0, 1.0, 13),
+    (11, 3, 2, 1.0, 2.0, 14),     # responses only: no prompt is ever queued
+    (13, 2, 3, 1.5, 1.0, 15),     # prompts only
 ]
 
 
-@pytest.mark.parametrize("n_prompts,P0,R0,eta,seed", CASES)
-def test_online_tail_batching_matches_plan_and_unscheduled_tokens(tiny, n_prompts, P0, R0, eta, seed):
+@pytest.mark.parametrize("n_prompts,P0,R0,eta_p,eta_r,seed", CASES)
+def test_online_tail_batching_matches_plan_and_unscheduled_tokens(tiny, n_prompts, P0, R0, eta_p, eta_r, seed):
     s, wd = tiny
     R = rp()
-    r_spec = math.ceil(eta * R0)
+    r_spec = math.ceil(eta_r * R0)
     b = make_rl_batch(s, n_prompts, r_spec, p_lo=8, p_hi=40, median=24, sigma_p=0.7, sigma_r=0.5, lo=1, hi=80,
                       seed=seed, sample_seed=5, temperature=1.0)
-    log(f"tail-batched tiny: prompts={n_prompts} P0={P0} R0={R0} eta={eta} seed={seed}")
+    log(f"tail-batched tiny: prompts={n_prompts} P0={P0} R0={R0} eta_p={eta_p} eta_r={eta_r} seed={seed}")
     eng = _engine(s, wd, max_seqs=64, pages=128)
     resp, glen, acc, kept, stats = eng.rollout_tail_batched(b.seq_ids, b.prompt_tokens, b.prompt_offsets,
-                                                            b.max_new, b.sample_seed, b.temperature, P0, R0, eta)
-    plan = osch.plan_tail_batching(b.max_new.tolist(), P0, R0, eta)
-    nat, nat_acc, nat_kept = R.rp_plan_tail_batching(b.max_new, P0, R0, eta)
+                                                            b.max_new, b.sample_seed, b.temperature, P0, R0, eta_p,
+                                                            eta_r)
+    plan = osch.plan_tail_batching(b.max_new.tolist(), P0, R0, eta_p, eta_r)
+    nat, nat_acc, nat_kept = R.rp_plan_tail_batching(b.max_new, P0, R0, eta_p, eta_r)
     # decisions
     assert len(stats) == len(plan) == len(nat)
     for k, (st, rnd) in enumerate(zip(stats, plan)):

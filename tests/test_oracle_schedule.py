@@ -35,34 +35,35 @@ def _simulate_short(lens, launched, P0, R0, eta):
         for p in sorted(newly):          # same-step completions: lower index first
             if len(done) < keep_n:
                 done.append(p)
-    return sorted(done), t, {p: sorted(finished[p])[:R0] for p in done}
+    # finished[p] is in finish order (by step, then response index): keep the first R0
+    return sorted(done), t, {p: sorted(finished[p][:R0]) for p in done}
 
 
 @pytest.mark.parametrize("seed", range(40))
 def test_short_round_matches_step_simulation(seed):
     rng = np.random.default_rng(seed)
     P0, R0 = int(rng.integers(1, 5)), int(rng.integers(1, 4))
-    eta = float(rng.choice([1.0, 1.25, 1.5, 2.0]))
-    n = math.ceil(eta * P0)
-    r_spec = math.ceil(eta * R0)
+    eta_p, eta_r = (float(rng.choice([1.0, 1.25, 1.5, 2.0])) for _ in range(2))
+    n = math.ceil(eta_p * P0)
+    r_spec = math.ceil(eta_r * R0)
     lens = rng.integers(1, 12, size=(n, r_spec)).tolist()
-    rnd = osch.short_round(lens, list(range(n)), P0, R0, eta)
-    acc, t, kept = _simulate_short(lens, list(range(n)), P0, R0, eta)
+    rnd = osch.short_round(lens, list(range(n)), P0, R0, eta_r)
+    acc, t, kept = _simulate_short(lens, list(range(n)), P0, R0, eta_r)
     assert rnd["accepted"] == acc and rnd["time"] == t
-    # kept responses: any R0 finished by the prompt's completion step are valid;
-    # the planner keeps the shortest with lower index first on ties
+    # kept responses: the first R0 to finish, lower index first among same-step finishes
     for p in acc:
-        assert sorted(lens[p][r] for r in rnd["kept"][p]) == sorted(lens[p][r] for r in kept[p])
+        assert rnd["kept"][p] == kept[p]
 
 
 @pytest.mark.parametrize("seed", range(20))
 def test_plan_invariants(seed):
     rng = np.random.default_rng(100 + seed)
-    P0, R0, eta = int(rng.integers(1, 6)), int(rng.integers(1, 5)), 1.25
+    P0, R0 = int(rng.integers(1, 6)), int(rng.integers(1, 5))
+    eta_p, eta_r = [(1.25, 1.25), (1.0, 1.5), (1.5, 1.0), (1.25, 2.0)][seed % 4]
     n = int(rng.integers(1, 40))
-    r_spec = math.ceil(eta * R0)
+    r_spec = math.ceil(eta_r * R0)
     lens = np.clip(np.rint(50 * np.exp(rng.standard_normal((n, r_spec)))), 1, 2000).astype(int).tolist()
-    rounds = osch.plan_tail_batching(lens, P0, R0, eta)
+    rounds = osch.plan_tail_batching(lens, P0, R0, eta_p, eta_r)
     seen = []
     queue_order = []
     for rnd in rounds:
@@ -75,11 +76,39 @@ def test_plan_invariants(seed):
             assert rnd["accepted"] == queue_order[:len(rnd["accepted"])]
             queue_order = queue_order[len(rnd["accepted"]):]
         else:
+            assert len(rnd["launched"]) <= math.ceil(eta_p * P0)
             assert len(rnd["accepted"]) == min(P0, len(rnd["launched"]))
             assert all(len(rnd["kept"][p]) == R0 for p in rnd["accepted"])
             assert all(t <= rnd["time"] for t in rnd["run"].values())
             queue_order += rnd["rejected"]
     assert sorted(seen) == list(range(n))            # every prompt exactly once
+
+
+def test_speculation_counts_read_decimal_factors():
+    assert osch.spec_count(1.25, 128) == 160 and osch.spec_count(1.25, 8) == 10
+    assert osch.spec_count(1.1, 10) == 11 and osch.spec_count(float(np.float32(1.1)), 10) == 11
+    assert osch.spec_count(1.0, 7) == 7 and osch.spec_count(1.01, 10) == 11
+
+
+def test_factor_one_on_both_sides_is_the_unscheduled_plan():
+    """With eta_p = eta_r = 1 nothing is speculative: each round is one unscheduled step."""
+    rng = np.random.default_rng(5)
+    lens = rng.integers(1, 100, size=(12, 3)).tolist()
+    tb = osch.plan_tail_batching(lens, 4, 3, 1.0)
+    un = osch.plan_unscheduled(lens, 4, 3)
+    assert [r["time"] for r in tb] == [r["time"] for r in un]
+    assert [r["accepted"] for r in tb] == [r["accepted"] for r in un]
+
+
+def test_response_only_speculation_never_queues():
+    """eta_p = 1 launches exactly P0 prompts, all accepted: no prompt reaches the long queue (section 6.3)."""
+    rng = np.random.default_rng(6)
+    lens = rng.integers(1, 500, size=(20, 6)).tolist()
+    rounds = osch.plan_tail_batching(lens, 5, 4, 1.0, 1.5)
+    assert all(r["kind"] == "short" and not r["rejected"] for r in rounds)
+    # each round ends when its slowest prompt has its 4 shortest of 6 responses
+    for r in rounds:
+        assert r["time"] == max(sorted(lens[p])[3] for p in r["launched"])
 
 
 def test_unscheduled_and_slot_idle():

@@ -286,12 +286,15 @@ def make_rl_batch(shape: ModelShape, n_prompts: int, r_spec: int, *, p_lo: int, 
 
     z_p is one standard normal draw per prompt (its difficulty: hard prompts give
     long responses across the board, as the paper observes in section 6.3) and
-    z_pr one per response.  Prompt lengths are U[p_lo, p_hi], ids U[0, vocab)."""
+    z_pr one per response.  Prompt lengths are U[p_lo, p_hi], ids U[0, vocab).
+    Response r's draws come from a stream of their own, so the first r
+    responses of every prompt are the same whatever r_spec is."""
     rng = np.random.Generator(np.random.Philox(seed))
     plen = rng.integers(p_lo, p_hi + 1, size=n_prompts)
     prompts = [rng.integers(0, shape.vocab, size=int(p)).astype(np.int32) for p in plen]
     z_p = rng.standard_normal(n_prompts)[:, None]
-    z_pr = rng.standard_normal((n_prompts, r_spec))
+    z_pr = np.stack([np.random.Generator(np.random.Philox(key=np.array([seed, 1 + r], np.uint64)))
+                     .standard_normal(n_prompts) for r in range(r_spec)], axis=1).reshape(n_prompts, r_spec)
     lens = np.clip(np.rint(median * np.exp(sigma_p * z_p + sigma_r * z_pr)), lo, hi).astype(np.int32)
     offs = np.zeros(n_prompts + 1, np.int64)
     offs[1:] = np.cumsum(plen)
