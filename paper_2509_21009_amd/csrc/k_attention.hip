@@ -4,12 +4,14 @@
 // head (the G query heads of a token, or G heads x floor(16/G) tokens in
 // prefill) and a range of KV tokens.  Per 32-token half page it computes
 // S^T = K Q^T as two 16x16 MFMA tiles, runs an online softmax in the log2
-// domain, and accumulates O^T = V^T P^T with MFMA.  A V page is stored as
-// two 32-token halves, each transposed ([hd][32 tokens]), so that one
-// half's V operands are a contiguous 8 KB run and both MFMA operands are read
-// as 16-byte pieces straight from HBM; the tokens are assigned to MFMA rows
-// so that each lane's softmax outputs are exactly the P^T operand it must
-// supply, with no data exchange between lanes.
+// domain, and accumulates O^T = V^T P^T with MFMA.  Both operands are read
+// as 16-byte pieces straight from HBM, each load instruction one contiguous
+// 1 KB run: a K page is stored in MFMA operand order (k_page_offset; the
+// queries use the same dimension order, so every dot product is unchanged),
+// and a V page as two 32-token halves, each transposed ([hd][32 tokens]).
+// The tokens are assigned to MFMA rows so that each lane's softmax outputs
+// are exactly the P^T operand it must supply, with no data exchange between
+// lanes.
 //
 // Decode splits each sequence's context into chunks (one work item each, with
 // a host-built descriptor) so that small batches with long contexts still
@@ -42,15 +44,16 @@ __device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, 
                                             const bf16x8_t (&qf)[HD / 32], int row_lim, int t_lo,
                                             int t_hi, float scale_log2, SoftmaxState& st,
                                             f32x4_t (&o)[HD / 16]) {
-  constexpr int KS = HD / 32, HQ = HD / 4;
+  constexpr int KS = HD / 32;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   f32x4_t sacc[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const bf16_t* krow = kb + tile_token(t, c) * HD + g * HQ;
+    // tile t = 2h + tt of the page: its k-step ks is the 1 KB run (t * KS + ks), lane (g, c) at (4c + g) * 8
+    const bf16_t* krow = kb + (t * KS * 16 + c) * 32 + g * 8;
     bf16x8_t kf[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf[ks] = load_bf16x8(krow + ks * 8);
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = load_bf16x8(krow + ks * 512);
     sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) sacc[t] = mfma16x16x32(kf[ks], qf[ks], sacc[t]);
@@ -108,7 +111,7 @@ __device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, 
 
 template <int HD>
 __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
-  constexpr int KS = HD / 32, HQ = HD / 4, NB = HD / 16, D = 2;
+  constexpr int KS = HD / 32, NB = HD / 16, D = 2;
   const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
   const int x = blockIdx.x, kh = blockIdx.y;
   const int4 dsc = reinterpret_cast<const int4*>(a.split_desc)[x];
@@ -118,10 +121,10 @@ __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
   const int G = a.n_q / a.n_kv;
 
   bf16x8_t qf[KS];
-  if (c < G) {
-    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (static_cast<size_t>(b) * a.n_q + kh * G + c) * HD + g * HQ;
+  if (c < G) {  // k-step ks, lane group g: dimensions 32ks + 8g .. +7, the K cache's order
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (static_cast<size_t>(b) * a.n_q + kh * G + c) * HD + g * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 8);
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 32);
   } else {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
@@ -147,10 +150,11 @@ __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
     const size_t pb = (static_cast<size_t>(pg) * a.n_kv + kh) * kPageTokens * HD;
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
-      // MFMA row c of S^T tile (2h + tt) of the page is token 32h + 8(c >> 2) + 4tt + (c & 3)
-      const bf16_t* krow = kpool + pb + (32 * h + 8 * (c >> 2) + 4 * tt + (c & 3)) * HD + g * HQ;
+      // MFMA row c of S^T tile (2h + tt) of the page is token 32h + 8(c >> 2) + 4tt + (c & 3);
+      // its k-step ks is the contiguous 1 KB run ((2h + tt) * KS + ks) of the page's K block
+      const bf16_t* krow = kpool + pb + (((2 * h + tt) * KS) * 16 + c) * 32 + g * 8;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kf[sl][tt][ks] = load_bf16x8(krow + ks * 8);
+      for (int ks = 0; ks < KS; ++ks) kf[sl][tt][ks] = load_bf16x8(krow + ks * 512);
     }
     const bf16_t* vh = vpool + pb + h * HD * 32;
 #pragma unroll
@@ -295,13 +299,23 @@ __global__ __launch_bounds__(HD * kMergeGroups) void k_attn_merge(AttnArgs a) {
   __syncthreads();
   mx = -INFINITY;
   for (int i = 0; i < HD * kMergeGroups / 64; ++i) mx = fmaxf(mx, wmax[i]);
+  // Split weights into LDS first, so that the loop below issues nothing but
+  // independent partial-output loads (unrolled 16 deep: a 256-split row takes
+  // two memory round trips per thread instead of one per few splits).
+  for (int t = threadIdx.x; t < nc; t += blockDim.x) sm[t] = (sm[t] == -INFINITY) ? 0.f : exp2f(sm[t] - mx);
+  __syncthreads();
+  const float* po = a.part_o + (static_cast<size_t>(s0) * a.n_kv + kh) * 16 * HD + c * HD + d;
+  const size_t po_stride = static_cast<size_t>(a.n_kv) * 16 * HD;  // one split
   float num = 0.f, den = 0.f;
-#pragma unroll 4
-  for (int t = q; t < n; t += kMergeGroups) {
-    const float ms = t < nc ? sm[t] : m_of(t);
+#pragma unroll 16
+  for (int t = q; t < nc; t += kMergeGroups) num += sm[t] * po[t * po_stride];
+  if (d == 0)
+    for (int t = q; t < nc; t += kMergeGroups) den += sm[t] * sl[t];
+  for (int t = nc + q; t < n; t += kMergeGroups) {  // splits beyond the LDS cache
+    const float ms = m_of(t);
     const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
-    num += w * a.part_o[((static_cast<size_t>(s0 + t) * a.n_kv + kh) * 16 + c) * HD + d];
-    if (d == 0) den += w * (t < nc ? sl[t] : l_of(t));
+    num += w * po[t * po_stride];
+    if (d == 0) den += w * l_of(t);
   }
   part_num[q][d] = num;
   if (d == 0) part_den[q] = den;
@@ -316,7 +330,7 @@ __global__ __launch_bounds__(HD * kMergeGroups) void k_attn_merge(AttnArgs a) {
 
 template <int HD>
 __global__ __launch_bounds__(64) void k_attn_prefill_bf16(AttnArgs a, int tpi) {
-  constexpr int KS = HD / 32, HQ = HD / 4;
+  constexpr int KS = HD / 32;
   const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
   const int x = blockIdx.x, kh = blockIdx.y;
   int lo = 0, hi = a.n_seq;
@@ -339,9 +353,9 @@ __global__ __launch_bounds__(64) void k_attn_prefill_bf16(AttnArgs a, int tpi) {
 
   bf16x8_t qf[KS];
   if (valid) {
-    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (qrow_idx * a.n_q + head) * HD + g * HQ;
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (qrow_idx * a.n_q + head) * HD + g * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 8);
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 32);
   } else {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));

@@ -166,9 +166,14 @@ __global__ __launch_bounds__(256) void k_rope_append(RopeArgs a) {
       Elem<T>::store(q, n2, r2);
     } else {
       const int kh = head - a.n_q;
-      const size_t base = ((static_cast<size_t>(page) * a.n_kv + kh) * kPageTokens + off) * hd;
-      Elem<T>::store(static_cast<T*>(a.k_pool), base + d, r1);
-      Elem<T>::store(static_cast<T*>(a.k_pool), base + d + half, r2);
+      const size_t blk = (static_cast<size_t>(page) * a.n_kv + kh) * kPageTokens * hd;
+      if (sizeof(T) == 2) {  // bf16 cache: MFMA operand order
+        Elem<T>::store(static_cast<T*>(a.k_pool), blk + k_page_offset(off, d, hd), r1);
+        Elem<T>::store(static_cast<T*>(a.k_pool), blk + k_page_offset(off, d + half, hd), r2);
+      } else {
+        Elem<T>::store(static_cast<T*>(a.k_pool), blk + static_cast<size_t>(off) * hd + d, r1);
+        Elem<T>::store(static_cast<T*>(a.k_pool), blk + static_cast<size_t>(off) * hd + d + half, r2);
+      }
     }
   } else {
     const int e = t - n_pairs;

@@ -5,8 +5,9 @@
 //   h      T    [M, H]               normalised GEMM input (T = float or bf16)
 //   part   fp32 [S, M, N]            split-K partial GEMM outputs, summed by the consumer
 //   q      T    [M, n_q, hd]         rotated queries
-//   K pool T    [layer][page][n_kv][64 tokens][hd]
-//   V pool T    [layer][page][n_kv][hd][64 tokens]   (transposed per page)
+//   K pool fp32 [layer][page][n_kv][64 tokens][hd]
+//          bf16 [layer][page][n_kv][64 x hd in MFMA operand order, k_page_offset]
+//   V pool T    [layer][page][n_kv][2 halves][hd][32 tokens]   (transposed per half page)
 //   page table int32 [slot][max_pages_per_seq]
 #pragma once
 
@@ -16,6 +17,21 @@
 namespace rollpack {
 
 constexpr int kPageTokens = 64;
+
+// Element offset of (token tok of the page, dimension d) inside one
+// (page, KV head) block of the bf16 K cache.  The block is stored in the
+// order the attention kernels feed it to v_mfma_f32_16x16x32_bf16 as the
+// 16-row operand: [half page h][tile tt][k-step ks][row c][lane group g][8],
+// where row c of tile tt of half h is token 32h + 8(c >> 2) + 4tt + (c & 3)
+// and k-step ks, group g hold dimensions 32ks + 8g .. 32ks + 8g + 7.  One
+// (h, tt, ks) triple is then one contiguous 1 KB run that a wave's single
+// 16-byte-per-lane load covers in whole 128-byte lines.
+__host__ __device__ __forceinline__ int k_page_offset(int tok, int d, int hd) {
+  const int h = tok >> 5, r = tok & 31;
+  const int tt = (r >> 2) & 1, c = ((r >> 3) << 2) | (r & 3);
+  const int ks = d >> 5, g = (d >> 3) & 3, e = d & 7;
+  return ((((h * 2 + tt) * (hd / 32) + ks) * 16 + c) * 4 + g) * 8 + e;
+}
 
 // Weight rows split over up to three tensors (q/k/v, or gate/up).  Each
 // segment holds `rows` rows of K elements; rows are multiples of 16.
