@@ -202,6 +202,23 @@ rp_status rp_abort(rp_engine* eng, int32_t n, const int64_t* seq_ids);
 rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t cap,
                         int32_t* len_out);
 
+/* The same for the log-probability of each generated token under the
+ * distribution it was sampled from, log softmax(logits / T)[token]
+ * (T = 1 for greedy sequences), as RL training needs for its importance
+ * ratios; fp32, from the logits the step computed. */
+rp_status rp_get_logprobs(rp_engine* eng, int64_t seq_id, float* out, int32_t cap,
+                          int32_t* len_out);
+
+/* End-of-sequence token (-1, the default: none).  A sequence that samples it
+ * stops there, the token included, before max_new_tokens.  The engine reads
+ * each step's sampled tokens two steps later, so that it never waits on the
+ * step just launched: a stopped sequence may take part in one more step,
+ * whose token is discarded, and is reported finished by rp_free_finished
+ * (which reads every pending check first).  Responses equal the forced-length
+ * ones cut after their first end-of-sequence token, since tokens are keyed by
+ * position.  The engine must have no live sequences (RP_ERR_BAD_STATE). */
+rp_status rp_set_eos(rp_engine* eng, int32_t eos_token);
+
 /* Whole-batch rollout: generate max_new_tokens[i] tokens for each of n
  * sequences, round by round (rounds in increasing round_ids order; NULL =
  * one round).  Within a round all sequences are admitted together (prefill
@@ -211,6 +228,11 @@ rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t ca
  *   round_ids       host [n] or NULL
  *   resp_tokens_out host [sum max_new_tokens]: sequence i's tokens at
  *                   offset sum_{j<i} max_new_tokens[j]
+ *   resp_logprobs_out host [sum max_new_tokens] or NULL: the log-probability
+ *                   of each token, laid out like the tokens (rp_get_logprobs)
+ *   resp_len_out    host [n] or NULL: tokens generated, max_new_tokens[i]
+ *                   unless the sequence stopped at the end-of-sequence token
+ *                   (rp_set_eos); entries past it are left untouched
  *   stats_out       host [max_stats] or NULL: one record per round, in order
  *   n_rounds_out    host or NULL
  * The engine must have no live sequences. */
@@ -218,6 +240,7 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
                               const int32_t* prompt_tokens, const int64_t* prompt_offsets,
                               const int32_t* max_new_tokens, uint64_t seed, float temperature,
                               const int32_t* round_ids, int32_t* resp_tokens_out,
+                              float* resp_logprobs_out, int32_t* resp_len_out,
                               rp_round_stats* stats_out, int32_t max_stats,
                               int32_t* n_rounds_out);
 
@@ -248,6 +271,7 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
  *   resp_tokens_out host [sum max_new_tokens]: response i's tokens at offset
  *                   sum_{j<i} max_new_tokens[j]; only its first resp_len_out[i]
  *                   entries are written
+ *   resp_logprobs_out host [sum max_new_tokens] or NULL: their log-probabilities
  *   resp_len_out    host [n_prompts * r_spec]: tokens the response generated in
  *                   the last round it ran in (0 if never launched)
  *   accept_round_out host [n_prompts]: round that accepted the prompt
@@ -262,7 +286,8 @@ rp_status rp_rollout_tail_batched(rp_engine* eng, int32_t n_prompts, int32_t r_s
                                   const int64_t* prompt_offsets, const int32_t* max_new_tokens,
                                   uint64_t seed, float temperature, int32_t P0, int32_t R0,
                                   float eta_p, float eta_r,
-                                  int32_t* resp_tokens_out, int32_t* resp_len_out,
+                                  int32_t* resp_tokens_out, float* resp_logprobs_out,
+                                  int32_t* resp_len_out,
                                   int32_t* accept_round_out, int32_t* kept_out,
                                   rp_round_stats* stats_out, int32_t max_stats,
                                   int32_t* n_rounds_out);

@@ -13,6 +13,13 @@ bits), so u lies in [2^-24, 1 - 2^-24].
 Temperature 0 is greedy argmax.  Ties go to the lowest vocabulary index.
 The logits/T + g sum and the argmax are taken in fp32, the precision of the
 kernel, since that arithmetic decides an integer.
+
+RL training needs the log-probability of each sampled token under the
+distribution it was drawn from: log softmax(logits / T)[token], computed here
+in fp64.  For greedy decoding (T = 0) the reported value is taken at T = 1.
+A response that stops at an end-of-sequence token is the forced-length
+response cut after the first occurrence of that token: tokens are keyed by
+position, so stopping changes nothing before it.
 """
 from __future__ import annotations
 
@@ -94,6 +101,20 @@ def scores(logits: np.ndarray, temperature: float, seed: int, seq_id: int, pos: 
 def sample(logits: np.ndarray, temperature: float, seed: int, seq_id: int, pos: int) -> int:
     """Token at absolute position ``pos``; lowest index wins ties (np.argmax)."""
     return int(np.argmax(scores(logits, temperature, seed, seq_id, pos)))
+
+
+def logprob(logits: np.ndarray, temperature: float, token: int) -> float:
+    """log softmax(logits / T)[token] in fp64 (T = 1 when T = 0)."""
+    t = 1.0 if temperature == 0.0 else float(temperature)
+    s = np.asarray(logits, np.float64) / t
+    m = float(np.max(s))
+    return float(s[token] - (m + np.log(np.sum(np.exp(s - m)))))
+
+
+def stop_at(tokens, eos: int):
+    """The response up to and including the first ``eos`` (all of it if there is none)."""
+    tokens = list(tokens)
+    return tokens[:tokens.index(eos) + 1] if eos in tokens else tokens
 
 
 def top2_gap(s: np.ndarray) -> float:

@@ -98,13 +98,17 @@ ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l) {
   p.page_table = take(S * p.max_pages * 4);
   p.tokens_cur = take(S * 4);
   p.hist = take(S * static_cast<size_t>(l.max_context) * 4);
+  p.logp = take(S * static_cast<size_t>(l.max_context) * 4);
   p.resp = take(S * static_cast<size_t>(l.max_context) * 4);
+  p.resp_logp = take(S * static_cast<size_t>(l.max_context) * 4);
   p.slot_seed = take(S * 8);
   p.slot_id = take(S * 8);
   p.slot_temp = take(S * 4);
   p.meta = take(static_cast<size_t>(p.meta_ints) * 4);
   p.cand_val = take(S * static_cast<size_t>(sample_chunks(c.vocab)) * 4);
   p.cand_idx = take(S * static_cast<size_t>(sample_chunks(c.vocab)) * 4);
+  p.cand_m = take(S * static_cast<size_t>(sample_chunks(c.vocab)) * 4);
+  p.cand_s = take(S * static_cast<size_t>(sample_chunks(c.vocab)) * 4);
   p.total = off;
   return p;
 }
@@ -190,6 +194,60 @@ Engine::~Engine() {
   if (h_slot_seed_) (void)hipHostFree(h_slot_seed_);
   if (h_slot_id_) (void)hipHostFree(h_slot_id_);
   if (h_slot_temp_) (void)hipHostFree(h_slot_temp_);
+  for (auto& c : eos_free_) {
+    (void)hipHostFree(c.host);
+    (void)hipEventDestroy(c.ev);
+  }
+  for (auto& c : eos_pending_) {
+    (void)hipHostFree(c.host);
+    (void)hipEventDestroy(c.ev);
+  }
+}
+
+void Engine::set_eos(int32_t token) {
+  if (token < -1 || token >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "end-of-sequence token out of range");
+  if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "the end-of-sequence token changes only with no live sequences");
+  eos_token_ = token;
+}
+
+void Engine::note_samples(const std::vector<std::array<int64_t, 3>>& rows) {
+  const int64_t step = sample_step_++;
+  for (const auto& r : rows) slots_[r[0]].last_step = step;
+  if (eos_token_ < 0 || rows.empty()) return;
+  EosCheck c;
+  if (!eos_free_.empty()) {
+    c = std::move(eos_free_.back());
+    eos_free_.pop_back();
+  } else {
+    HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c.host), static_cast<size_t>(lim_.max_seqs) * 4,
+                          hipHostMallocDefault));
+    HIP_TRY(hipEventCreateWithFlags(&c.ev, hipEventDisableTiming));
+  }
+  c.step = step;
+  c.rows = rows;
+  HIP_TRY(hipMemcpyAsync(c.host, scratch_ + plan_.tokens_cur, static_cast<size_t>(lim_.max_seqs) * 4,
+                         hipMemcpyDeviceToHost, stream_));
+  HIP_TRY(hipEventRecord(c.ev, stream_));
+  eos_pending_.push_back(std::move(c));
+}
+
+void Engine::apply_eos(int64_t upto) {
+  while (!eos_pending_.empty() && eos_pending_.front().step <= upto) {
+    EosCheck& c = eos_pending_.front();
+    HIP_TRY(hipEventSynchronize(c.ev));
+    for (const auto& r : c.rows) {
+      const int32_t slot = static_cast<int32_t>(r[0]);
+      Seq& q = slots_[slot];
+      if (!q.live || q.id != r[1] || q.stopped || c.host[slot] != eos_token_) continue;
+      q.stopped = true;
+      q.finished = true;
+      q.n_gen = std::min<int32_t>(q.n_gen, static_cast<int32_t>(r[2]) + 1);
+    }
+    eos_applied_ = c.step;
+    eos_free_.push_back(std::move(c));
+    eos_pending_.pop_front();
+  }
+  if (eos_pending_.empty()) eos_applied_ = sample_step_ - 1;
 }
 
 int32_t* Engine::stage_meta(size_t ints) {
@@ -426,8 +484,9 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
 
   SampleArgs sa{sp<float>(plan_.logits), m_lm, V, m_gen_slot_, m_gen_pos_, m_gen_hist_,
                 sp<uint64_t>(plan_.slot_seed), sp<uint64_t>(plan_.slot_id), sp<float>(plan_.slot_temp),
-                tokens_cur, sp<int32_t>(plan_.hist), lim_.max_context, sp<float>(plan_.cand_val),
-                sp<int32_t>(plan_.cand_idx)};
+                tokens_cur, sp<int32_t>(plan_.hist), lim_.max_context, sp<float>(plan_.logp),
+                sp<float>(plan_.cand_val), sp<int32_t>(plan_.cand_idx), sp<float>(plan_.cand_m),
+                sp<float>(plan_.cand_s)};
   launch_timed(RP_K_SAMPLE, static_cast<double>(m_lm) * V * 4, 0, [&] { return launch_sample(sa, s); });
 }
 
@@ -481,6 +540,10 @@ void Engine::run_prefill_chunk(const std::vector<PrefillPiece>& pcs, float* logi
   m_seq_ntok_ = m_seq_pos0_ + n; m_item_off_ = m_seq_ntok_ + n; m_last_row_ = m_item_off_ + n + 1;
   m_gen_pos_ = m_last_row_ + n; m_gen_hist_ = m_gen_pos_ + n; m_gen_slot_ = m_seq_slot_;
   forward(T, true, n, items, 0, 0);
+  std::vector<std::array<int64_t, 3>> sampled;  // pieces that end their sequence sampled its next token
+  for (const PrefillPiece& pc : pcs)
+    if (pc.seq >= 0) sampled.push_back({pc.slot, slots_[pc.slot].id, pc.hist0});
+  note_samples(sampled);
   if (logits_out) {
     // logits rows of the pieces that end a sequence, in runs of consecutive sequences
     int j = 0;
@@ -496,7 +559,7 @@ void Engine::run_prefill_chunk(const std::vector<PrefillPiece>& pcs, float* logi
   }
 }
 
-std::vector<int32_t> Engine::admit_seqs(const std::vector<AdmitSeq>& a, const std::vector<const int32_t*>& restore,
+std::vector<int32_t> Engine::admit_seqs(const std::vector<AdmitSeq>& a, const std::vector<const Waiting*>& restore,
                                         float* logits_out) {
   const int32_t n = static_cast<int32_t>(a.size());
   if (tables_pending_) {
@@ -530,12 +593,16 @@ std::vector<int32_t> Engine::admit_seqs(const std::vector<AdmitSeq>& a, const st
     new_slots[i] = s;
   }
   upload_slot_tables();
-  // Tokens a resumed sequence generated before its preemption go back into its history row.
+  // Tokens (and their log-probabilities) a resumed sequence generated before
+  // its preemption go back into its history rows.
   bool restored = false;
   for (int32_t i = 0; i < n; ++i)
     if (a[i].n_gen0 > 0 && restore[i]) {
-      HIP_TRY(hipMemcpyAsync(sp<int32_t>(plan_.hist) + static_cast<size_t>(new_slots[i]) * lim_.max_context,
-                             restore[i], static_cast<size_t>(a[i].n_gen0) * 4, hipMemcpyHostToDevice, stream_));
+      const size_t at = static_cast<size_t>(new_slots[i]) * lim_.max_context;
+      HIP_TRY(hipMemcpyAsync(sp<int32_t>(plan_.hist) + at, restore[i]->tokens.data() + restore[i]->prompt_len,
+                             static_cast<size_t>(a[i].n_gen0) * 4, hipMemcpyHostToDevice, stream_));
+      HIP_TRY(hipMemcpyAsync(sp<float>(plan_.logp) + at, restore[i]->logp.data(),
+                             static_cast<size_t>(a[i].n_gen0) * 4, hipMemcpyHostToDevice, stream_));
       restored = true;
     }
   if (restored) HIP_TRY(hipStreamSynchronize(stream_));
@@ -582,7 +649,7 @@ void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const i
     const int32_t p = static_cast<int32_t>(offs[i + 1] - offs[i]);
     a[i] = AdmitSeq{ids[i], toks + offs[i], p, p, max_new[i], 0, seed, temp, arrival_next_++};
   }
-  const std::vector<int32_t> new_slots = admit_seqs(a, std::vector<const int32_t*>(n, nullptr), logits_out);
+  const std::vector<int32_t> new_slots = admit_seqs(a, std::vector<const Waiting*>(n, nullptr), logits_out);
   if (first_out) {
     HIP_TRY(hipStreamSynchronize(stream_));
     std::vector<int32_t> cur(lim_.max_seqs);
@@ -594,6 +661,7 @@ void Engine::prefill(int32_t n, const int64_t* ids, const int32_t* toks, const i
 int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* row_ids_out) {
   if (forced && kv_policy_ == RP_KV_ON_DEMAND)
     throw RpError(RP_ERR_INVALID_ARG, "teacher forcing needs the reserving KV policy");
+  if (eos_token_ >= 0) apply_eos(sample_step_ - 2);  // the step before last has finished by now
   std::vector<int32_t> resumed;
   if (kv_policy_ == RP_KV_ON_DEMAND) resumed = schedule_pages();
   std::vector<int32_t> rows;
@@ -668,6 +736,9 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     HIP_TRY(hipMemcpyAsync(logits_out, scratch_ + plan_.logits, static_cast<size_t>(B) * cfg_.vocab * 4,
                            hipMemcpyDeviceToDevice, stream_));
   }
+  std::vector<std::array<int64_t, 3>> sampled(B);
+  for (int i = 0; i < B; ++i) sampled[i] = {rows[i], slots_[rows[i]].id, slots_[rows[i]].n_gen};
+  note_samples(sampled);
   for (int i = 0; i < B; ++i) {
     Seq& q = slots_[rows[i]];
     if (row_ids_out) row_ids_out[i] = q.id;
@@ -708,6 +779,7 @@ void Engine::release(int32_t slot) {
 }
 
 int32_t Engine::free_finished(int64_t* ids_out, int32_t cap) {
+  drain_eos();
   std::vector<int32_t> fin;
   for (int32_t s : order_)
     if (slots_[s].finished && static_cast<int32_t>(fin.size()) < cap) fin.push_back(s);
@@ -756,9 +828,12 @@ void Engine::preempt(const std::vector<int32_t>& victims) {
   HIP_TRY(hipStreamSynchronize(stream_));  // the history rows hold the last sampled tokens
   for (int32_t s : victims) {
     const Seq& q = slots_[s];
-    Waiting w{q.id, q.prompt_len, q.max_new, q.n_gen, q.seed, q.temp, q.arrival, q.prompt};
+    Waiting w{q.id, q.prompt_len, q.max_new, q.n_gen, q.seed, q.temp, q.arrival, q.prompt, {}};
     w.tokens.resize(static_cast<size_t>(q.prompt_len) + q.n_gen);
+    w.logp.resize(static_cast<size_t>(q.n_gen));
     HIP_TRY(hipMemcpy(w.tokens.data() + q.prompt_len, sp<int32_t>(plan_.hist) + static_cast<size_t>(s) * lim_.max_context,
+                      static_cast<size_t>(q.n_gen) * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(w.logp.data(), sp<float>(plan_.logp) + static_cast<size_t>(s) * lim_.max_context,
                       static_cast<size_t>(q.n_gen) * 4, hipMemcpyDeviceToHost));
     release(s);
     waiting_.insert(std::upper_bound(waiting_.begin(), waiting_.end(), w.arrival,
@@ -785,7 +860,7 @@ std::vector<int32_t> Engine::schedule_pages() {
   // Resume preempted sequences, oldest arrival first, while the pool has
   // room for them beyond what the running rows need this step.
   std::vector<AdmitSeq> adm;
-  std::vector<const int32_t*> restore;
+  std::vector<const Waiting*> restore;
   std::vector<Waiting> taken;
   int64_t reserve = need;
   size_t k = 0;
@@ -804,13 +879,20 @@ std::vector<int32_t> Engine::schedule_pages() {
       const int32_t ntok = w.prompt_len + w.n_gen;
       adm.push_back(AdmitSeq{w.id, w.tokens.data(), ntok, w.prompt_len, w.max_new, w.n_gen, w.seed, w.temp,
                              w.arrival});
-      restore.push_back(w.tokens.data() + w.prompt_len);
+      restore.push_back(&w);
       n_recompute_tok_ += ntok;
     }
   }
   std::vector<int32_t> resumed;
   if (!adm.empty()) resumed = admit_seqs(adm, restore, nullptr);
-  // Preempt the latest arrivals until the remaining rows fit.
+  // Preempt the latest arrivals until the remaining rows fit (after reading
+  // every pending end-of-sequence check, so that no stopped row is chosen).
+  if (need > pool_.free_pages() && eos_token_ >= 0) {
+    drain_eos();
+    need = 0;
+    rows.erase(std::remove_if(rows.begin(), rows.end(), [&](int32_t s) { return slots_[s].finished; }), rows.end());
+    for (int32_t s : rows) need += extra(s);
+  }
   std::vector<int32_t> victims;
   while (need > pool_.free_pages()) {
     if (rows.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "KV pool held by finished sequences; free them first");
@@ -851,12 +933,36 @@ int32_t Engine::get_tokens(int64_t id, int32_t* out, int32_t cap) {
   }
   auto it = id2slot_.find(id);
   if (it == id2slot_.end()) throw RpError(RP_ERR_UNKNOWN_ID, "get_tokens: unknown sequence id");
-  const Seq& q = slots_[it->second];
   HIP_TRY(hipStreamSynchronize(stream_));
+  drain_eos();
+  const Seq& q = slots_[it->second];
   const int32_t k = std::min(cap, q.n_gen);
   if (k > 0) {
     if (!out) throw RpError(RP_ERR_INVALID_ARG, "get_tokens: null output");
     HIP_TRY(hipMemcpy(out, sp<int32_t>(plan_.hist) + static_cast<size_t>(it->second) * lim_.max_context, k * 4,
+                      hipMemcpyDeviceToHost));
+  }
+  return q.n_gen;
+}
+
+int32_t Engine::get_logprobs(int64_t id, float* out, int32_t cap) {
+  if (const Waiting* w = find_waiting(id)) {
+    const int32_t k = std::min(cap, w->n_gen);
+    if (k > 0) {
+      if (!out) throw RpError(RP_ERR_INVALID_ARG, "get_logprobs: null output");
+      std::copy(w->logp.begin(), w->logp.begin() + k, out);
+    }
+    return w->n_gen;
+  }
+  auto it = id2slot_.find(id);
+  if (it == id2slot_.end()) throw RpError(RP_ERR_UNKNOWN_ID, "get_logprobs: unknown sequence id");
+  HIP_TRY(hipStreamSynchronize(stream_));
+  drain_eos();
+  const Seq& q = slots_[it->second];
+  const int32_t k = std::min(cap, q.n_gen);
+  if (k > 0) {
+    if (!out) throw RpError(RP_ERR_INVALID_ARG, "get_logprobs: null output");
+    HIP_TRY(hipMemcpy(out, sp<float>(plan_.logp) + static_cast<size_t>(it->second) * lim_.max_context, k * 4,
                       hipMemcpyDeviceToHost));
   }
   return q.n_gen;
@@ -896,7 +1002,9 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
                        int32_t* gen_out, Race* race, rp_round_stats* st) {
   const size_t resp_cap = static_cast<size_t>(lim_.max_seqs) * lim_.max_context;
   int32_t* resp_dev = sp<int32_t>(plan_.resp);
+  float* resp_logp_dev = sp<float>(plan_.resp_logp);
   const int32_t* hist = sp<int32_t>(plan_.hist);
+  const float* logp_hist = sp<float>(plan_.logp);
   size_t next = 0;
   size_t n_ev = 0;
   hipEvent_t ev_start = event_at(n_ev++);
@@ -931,8 +1039,12 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
   auto flush = [&]() {
     if (pending_copies.empty()) return;
     HIP_TRY(hipStreamSynchronize(stream_));
-    for (auto& c : pending_copies)
+    for (auto& c : pending_copies) {
       HIP_TRY(hipMemcpy(resp_out + c[1], resp_dev + c[0], static_cast<size_t>(c[2]) * 4, hipMemcpyDeviceToHost));
+      if (a.logp_out)
+        HIP_TRY(hipMemcpy(a.logp_out + c[1], resp_logp_dev + c[0], static_cast<size_t>(c[2]) * 4,
+                          hipMemcpyDeviceToHost));
+    }
     pending_copies.clear();
     resp_cursor = 0;
   };
@@ -968,6 +1080,9 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     if (resp_cursor + len > resp_cap) flush();
     HIP_TRY(hipMemcpyAsync(resp_dev + resp_cursor, hist + static_cast<size_t>(s) * lim_.max_context, len * 4,
                            hipMemcpyDeviceToDevice, stream_));
+    if (a.logp_out)
+      HIP_TRY(hipMemcpyAsync(resp_logp_dev + resp_cursor, logp_hist + static_cast<size_t>(s) * lim_.max_context,
+                             len * 4, hipMemcpyDeviceToDevice, stream_));
     pending_copies.push_back({static_cast<int64_t>(resp_cursor), a.resp_off[i], len});
     resp_cursor += len;
     if (gen_out) gen_out[i] = static_cast<int32_t>(len);
@@ -981,6 +1096,7 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     const int32_t k = id_member.at(w.id);
     const int32_t i = members[k];
     std::copy(w.tokens.begin() + w.prompt_len, w.tokens.end(), resp_out + a.resp_off[i]);
+    if (a.logp_out) std::copy(w.logp.begin(), w.logp.end(), a.logp_out + a.resp_off[i]);
     if (gen_out) gen_out[i] = w.n_gen;
     left_ev.push_back({n_ev, k});
     gen_tokens += w.n_gen;
@@ -994,7 +1110,7 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
       // Completions of this step, in member order (responses of a prompt by index).
       std::vector<std::pair<int32_t, int32_t>> fin;  // (member, prompt)
       for (int32_t s : order_)
-        if (slots_[s].finished) {
+        if (slots_[s].finished && settled(slots_[s])) {
           const int32_t k = id_member.at(slots_[s].id);
           fin.push_back({k, race->prompt[k]});
         }
@@ -1019,9 +1135,12 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
       }
       stop = n_acc >= race->keep;
     }
+    // Sequences about to be aborted take their pending end-of-sequence checks first.
+    if (race && eos_token_ >= 0 && (stop || std::find(abort_prompt.begin(), abort_prompt.end(), 1) != abort_prompt.end()))
+      drain_eos();
     auto goes = [&](int64_t id) { return stop || (race && abort_prompt[race->prompt[id_member.at(id)]]); };
     for (int32_t s : order_)
-      if (slots_[s].finished || goes(slots_[s].id)) leaving.push_back(s);
+      if ((slots_[s].finished && settled(slots_[s])) || goes(slots_[s].id)) leaving.push_back(s);
     bool any = !leaving.empty();
     for (int32_t s : leaving) retire(s);
     if (race) {
@@ -1053,8 +1172,10 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     }
     if (order_.empty() && waiting_.empty() && next >= members.size()) break;
     if (order_.empty() && waiting_.empty()) throw RpError(RP_ERR_OUT_OF_PAGES, "rollout: a sequence cannot be admitted");
-    decode_step(nullptr, nullptr, nullptr);
-    ++steps;
+    if (decode_step(nullptr, nullptr, nullptr) > 0)
+      ++steps;
+    else
+      drain_eos();  // only finished sequences are left: settle their end-of-sequence checks
     collect();
   }
   HIP_TRY(hipEventRecord(ev_end, stream_));
@@ -1091,7 +1212,8 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
 
 int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
                         const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
-                        int32_t* resp_out, rp_round_stats* stats, int32_t max_stats) {
+                        int32_t* resp_out, float* logp_out, int32_t* len_out, rp_round_stats* stats,
+                        int32_t max_stats) {
   if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
   if (n < 1 || !ids || !toks || !offs || !max_new || !resp_out)
     throw RpError(RP_ERR_INVALID_ARG, "rollout: null array or n < 1");
@@ -1099,12 +1221,12 @@ int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, cons
   validate_seqs(n, ids, toks, offs, max_new, temp, resp_off);
   std::map<int32_t, std::vector<int32_t>> rounds;
   for (int32_t i = 0; i < n; ++i) rounds[round_ids ? round_ids[i] : 0].push_back(i);
-  const SeqArrays arr{ids, toks, offs, max_new, resp_off.data(), seed, temp};
+  const SeqArrays arr{logp_out, ids, toks, offs, max_new, resp_off.data(), seed, temp};
   int32_t r_idx = 0;
   for (auto& kv : rounds) {
     rp_round_stats st{};
     st.round_id = kv.first;
-    run_round(kv.second, arr, resp_out, nullptr, nullptr, &st);
+    run_round(kv.second, arr, resp_out, len_out, nullptr, &st);
     if (stats && r_idx < max_stats) stats[r_idx] = st;
     ++r_idx;
   }
@@ -1114,7 +1236,7 @@ int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, cons
 int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const int64_t* ids, const int32_t* ptoks,
                                      const int64_t* poffs, const int32_t* max_new, uint64_t seed, float temp,
                                      int32_t P0, int32_t R0, float eta_p, float eta_r, int32_t* resp_out,
-                                     int32_t* gen_out,
+                                     float* logp_out, int32_t* gen_out,
                                      int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
                                      int32_t max_stats) {
   if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "rollout needs an engine without live sequences");
@@ -1159,7 +1281,7 @@ int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const in
       throw RpError(RP_ERR_CAPACITY, "a short round's responses do not fit max_seqs or the KV pool together");
   }
 
-  const SeqArrays arr{ids, toks.data(), offs.data(), max_new, resp_off.data(), seed, temp};
+  const SeqArrays arr{logp_out, ids, toks.data(), offs.data(), max_new, resp_off.data(), seed, temp};
   for (int32_t p = 0; p < n_prompts; ++p) accept_round_out[p] = -1;
   for (int32_t i = 0; i < n; ++i) kept_out[i] = 0, gen_out[i] = 0;
   std::deque<int32_t> queue;  // prompts aborted by short rounds, oldest first

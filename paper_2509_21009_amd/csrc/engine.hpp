@@ -3,7 +3,9 @@
 
 #include <hip/hip_runtime.h>
 
+#include <array>
 #include <cstdint>
+#include <deque>
 #include <stdexcept>
 #include <string>
 #include <unordered_map>
@@ -23,7 +25,8 @@ struct RpError : std::runtime_error {
 // Byte offsets of every buffer carved from the caller's scratch workspace.
 struct ScratchPlan {
   size_t x, h, part, q, attn, act, hsel, logits, att_o, att_ml, rope_cos, rope_sin, page_table,
-      tokens_cur, hist, resp, slot_seed, slot_id, slot_temp, meta, cand_val, cand_idx;
+      tokens_cur, hist, logp, resp, resp_logp, slot_seed, slot_id, slot_temp, meta, cand_val, cand_idx, cand_m,
+      cand_s;
   size_t total;
   size_t part_elems;
   int32_t split_cap;   // decode attention work-item capacity (splits)
@@ -46,6 +49,8 @@ struct Seq {
   bool live = false;
   bool finished = false;
   int64_t arrival = 0;   // admission order of the sequence's first prefill
+  bool stopped = false;  // ended by the end-of-sequence token
+  int64_t last_step = -1;  // sample step that produced its latest token
   std::vector<int32_t> pages;
   std::vector<int32_t> prompt;  // kept under on-demand pages, for a recompute after preemption
 };
@@ -59,6 +64,7 @@ struct Waiting {
   float temp;
   int64_t arrival;
   std::vector<int32_t> tokens;  // prompt followed by the n_gen generated tokens
+  std::vector<float> logp;      // log-probabilities of the n_gen generated tokens
 };
 
 // One sequence to (re)admit: prefill `ntok` tokens at positions 0..ntok-1 and
@@ -82,6 +88,7 @@ struct PrefillPiece {
 
 // Per-sequence inputs of one rollout call (prompt CSR per sequence).
 struct SeqArrays {
+  float* logp_out;          // host, nullable: log-probabilities laid out like the tokens
   const int64_t* ids;
   const int32_t* toks;
   const int64_t* offs;
@@ -113,13 +120,16 @@ class Engine {
   int32_t free_finished(int64_t* ids_out, int32_t cap);
   void abort(int32_t n, const int64_t* ids);
   int32_t get_tokens(int64_t id, int32_t* out, int32_t cap);
+  int32_t get_logprobs(int64_t id, float* out, int32_t cap);
+  void set_eos(int32_t token);
   int32_t rollout(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
                   const int32_t* max_new, uint64_t seed, float temp, const int32_t* round_ids,
-                  int32_t* resp_out, rp_round_stats* stats, int32_t max_stats);
+                  int32_t* resp_out, float* logp_out, int32_t* len_out, rp_round_stats* stats,
+                  int32_t max_stats);
   int32_t rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const int64_t* ids, const int32_t* ptoks,
                                const int64_t* poffs, const int32_t* max_new, uint64_t seed, float temp,
                                int32_t P0, int32_t R0, float eta_p, float eta_r, int32_t* resp_out,
-                               int32_t* gen_out,
+                               float* logp_out, int32_t* gen_out,
                                int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
                                int32_t max_stats);
 
@@ -149,7 +159,7 @@ class Engine {
   // Pages a sequence takes at admission: its whole length when reserving,
   // else the tokens to prefill (on demand).
   int64_t admit_pages(int64_t prompt_len, int64_t max_new, int64_t ntok) const;
-  std::vector<int32_t> admit_seqs(const std::vector<AdmitSeq>& a, const std::vector<const int32_t*>& restore,
+  std::vector<int32_t> admit_seqs(const std::vector<AdmitSeq>& a, const std::vector<const Waiting*>& restore,
                                   float* logits_out);
   void run_prefill_chunk(const std::vector<PrefillPiece>& pcs, float* logits_out);
   // On-demand pages: resume waiting sequences that fit, then give every
@@ -157,6 +167,14 @@ class Engine {
   // when the pool runs dry.  Returns the slots resumed (they advanced already).
   std::vector<int32_t> schedule_pages();
   void preempt(const std::vector<int32_t>& victims);
+  // End-of-sequence checks: after each sampler launch the sampled tokens are
+  // copied to pinned memory; they are read two sample steps later (or when
+  // the caller needs final state), so the host never waits on the step it
+  // just launched.  A sequence that sampled the token is cut after it.
+  void note_samples(const std::vector<std::array<int64_t, 3>>& rows);  // (slot, id, history index)
+  void apply_eos(int64_t upto);
+  void drain_eos() { apply_eos(sample_step_ - 1); }
+  bool settled(const Seq& q) const { return eos_token_ < 0 || q.last_step <= eos_applied_; }
   bool known_id(int64_t id) const;
   Waiting* find_waiting(int64_t id);
   void release(int32_t slot);
@@ -191,6 +209,17 @@ class Engine {
   int32_t kv_policy_ = RP_KV_RESERVE;
   int64_t arrival_next_ = 0;
   int64_t n_preempt_ = 0, n_recompute_tok_ = 0;
+  struct EosCheck {
+    int64_t step;
+    hipEvent_t ev;
+    int32_t* host;  // pinned copy of tokens_cur
+    std::vector<std::array<int64_t, 3>> rows;
+  };
+  int32_t eos_token_ = -1;
+  int64_t sample_step_ = 0;   // sampler launches so far
+  int64_t eos_applied_ = -1;  // every sample step up to this one has been checked
+  std::deque<EosCheck> eos_pending_;
+  std::vector<EosCheck> eos_free_;
   std::unordered_map<int64_t, int32_t> id2slot_;
   // pinned host mirrors
   int32_t* h_page_table_ = nullptr;

@@ -220,13 +220,25 @@ __device__ __forceinline__ void take_best(float& bv, int& bi, float v, int i) {
   if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
 }
 
+// Running log-sum-exp state (max m, sum of exp(x - m)); combining two states
+// rescales the smaller-max sum.
+__device__ __forceinline__ void lse_add(float& m, float& s, float x) {
+  if (x > m) { s = s * expf(m - x) + 1.f; m = x; } else { s += expf(x - m); }
+}
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  if (m2 == -INFINITY) return;
+  if (m2 > m) { s = s * expf(m - m2) + s2; m = m2; } else { s += s2 * expf(m2 - m); }
+}
+
 // Pass 1: block (row, chunk) scores kSampleChunk vocabulary entries and
-// writes its best (score, index).  Pass 2: one wave per row reduces the
-// chunk winners (ties -> lowest index) and records the token.
+// writes its best (score, index) and the log-sum-exp state of logits / T
+// over the chunk.  Pass 2: one wave per row reduces the chunk winners (ties
+// -> lowest index), records the token and its log-probability
+// logits[token] / T - logsumexp(logits / T) (T = 1 for greedy rows).
 constexpr int kSampleChunk = 2048;
 
 __global__ __launch_bounds__(256) void k_sample_partial(SampleArgs a) {
-  __shared__ float sv[4];
+  __shared__ float sv[4], sm[4], ss[4];
   __shared__ int si[4];
   const int row = blockIdx.x;
   const int slot = a.row_slot[row];
@@ -234,12 +246,16 @@ __global__ __launch_bounds__(256) void k_sample_partial(SampleArgs a) {
   const float* l = a.logits + static_cast<size_t>(row) * a.V;
   float best = -INFINITY;
   int besti = 0x7fffffff;
+  float lm = -INFINITY, ls = 0.f;  // log-sum-exp state of logits / T
   const int v0 = blockIdx.y * kSampleChunk;
   if (temp == 0.f) {
 #pragma unroll
     for (int e = 0; e < kSampleChunk / 256; ++e) {
       const int v = v0 + e * 256 + threadIdx.x;
-      if (v < a.V) take_best(best, besti, l[v], v);
+      if (v < a.V) {
+        take_best(best, besti, l[v], v);
+        lse_add(lm, ls, l[v]);
+      }
     }
   } else {
     const float inv_t = 1.0f / temp;
@@ -257,6 +273,7 @@ __global__ __launch_bounds__(256) void k_sample_partial(SampleArgs a) {
         if (vb + e < a.V) {
           const uint32_t w = (e & 1) ? static_cast<uint32_t>(outs[e >> 1] >> 32) : static_cast<uint32_t>(outs[e >> 1]);
           take_best(best, besti, lv[e] * inv_t + word_to_gumbel(w), vb + e);
+          lse_add(lm, ls, lv[e] * inv_t);
         }
       }
     }
@@ -266,13 +283,25 @@ __global__ __launch_bounds__(256) void k_sample_partial(SampleArgs a) {
     const float ov = __shfl_xor(best, m, 64);
     const int oi = __shfl_xor(besti, m, 64);
     take_best(best, besti, ov, oi);
+    const float om = __shfl_xor(lm, m, 64);
+    const float os = __shfl_xor(ls, m, 64);
+    lse_merge(lm, ls, om, os);
   }
-  if ((threadIdx.x & 63) == 0) { sv[threadIdx.x >> 6] = best; si[threadIdx.x >> 6] = besti; }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = best; si[threadIdx.x >> 6] = besti;
+    sm[threadIdx.x >> 6] = lm; ss[threadIdx.x >> 6] = ls;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w) take_best(best, besti, sv[w], si[w]);
-    a.cand_val[static_cast<size_t>(row) * gridDim.y + blockIdx.y] = best;
-    a.cand_idx[static_cast<size_t>(row) * gridDim.y + blockIdx.y] = besti;
+    for (int w = 1; w < 4; ++w) {
+      take_best(best, besti, sv[w], si[w]);
+      lse_merge(lm, ls, sm[w], ss[w]);
+    }
+    const size_t c = static_cast<size_t>(row) * gridDim.y + blockIdx.y;
+    a.cand_val[c] = best;
+    a.cand_idx[c] = besti;
+    a.cand_m[c] = lm;
+    a.cand_s[c] = ls;
   }
 }
 
@@ -280,19 +309,31 @@ __global__ __launch_bounds__(64) void k_sample_final(SampleArgs a, int chunks) {
   const int row = blockIdx.x;
   float best = -INFINITY;
   int besti = 0x7fffffff;
-  for (int c = threadIdx.x; c < chunks; c += 64)
-    take_best(best, besti, a.cand_val[static_cast<size_t>(row) * chunks + c], a.cand_idx[static_cast<size_t>(row) * chunks + c]);
+  float lm = -INFINITY, ls = 0.f;
+  for (int c = threadIdx.x; c < chunks; c += 64) {
+    const size_t i = static_cast<size_t>(row) * chunks + c;
+    take_best(best, besti, a.cand_val[i], a.cand_idx[i]);
+    lse_merge(lm, ls, a.cand_m[i], a.cand_s[i]);
+  }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
     const float ov = __shfl_xor(best, m, 64);
     const int oi = __shfl_xor(besti, m, 64);
     take_best(best, besti, ov, oi);
+    const float om = __shfl_xor(lm, m, 64);
+    const float os = __shfl_xor(ls, m, 64);
+    lse_merge(lm, ls, om, os);
   }
   if (threadIdx.x == 0) {
     if (besti == 0x7fffffff) besti = 0;  // all-NaN row: deterministic fallback
     const int slot = a.row_slot[row];
+    const float temp = a.slot_temp[slot];
+    const float inv_t = temp == 0.f ? 1.f : 1.0f / temp;
+    const float s_tok = a.logits[static_cast<size_t>(row) * a.V + besti] * inv_t;
+    const size_t h = static_cast<size_t>(slot) * a.hist_stride + a.row_hist[row];
     a.tokens_cur[slot] = besti;
-    a.hist[static_cast<size_t>(slot) * a.hist_stride + a.row_hist[row]] = besti;
+    a.hist[h] = besti;
+    a.logp_hist[h] = s_tok - (lm + logf(ls));
   }
 }
 

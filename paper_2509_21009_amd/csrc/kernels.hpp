@@ -122,7 +122,9 @@ struct SampleArgs {
   const int32_t* row_hist;        // [B] index into the slot's token history
   const uint64_t* slot_seed; const uint64_t* slot_id; const float* slot_temp;
   int32_t* tokens_cur; int32_t* hist; int64_t hist_stride;
+  float* logp_hist;                     // [slots, hist_stride] log-probability of each sampled token
   float* cand_val; int32_t* cand_idx;   // [B, sample_chunks(V)] per-chunk winners
+  float* cand_m; float* cand_s;         // [B, sample_chunks(V)] per-chunk max and sum of exp(s - max)
 };
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
 int sample_chunks(int V);

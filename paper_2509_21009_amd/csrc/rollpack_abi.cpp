@@ -135,10 +135,12 @@ rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t ca
 rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
                               const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed,
                               float temperature, const int32_t* round_ids, int32_t* resp_tokens_out,
-                              rp_round_stats* stats_out, int32_t max_stats, int32_t* n_rounds_out) {
+                              float* resp_logprobs_out, int32_t* resp_len_out, rp_round_stats* stats_out,
+                              int32_t max_stats, int32_t* n_rounds_out) {
   return engine_call(eng, [&](rollpack::Engine* e) {
+    if (max_stats < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "max_stats must be >= 0");
     const int32_t r = e->rollout(n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
-                                 round_ids, resp_tokens_out, stats_out, max_stats);
+                                 round_ids, resp_tokens_out, resp_logprobs_out, resp_len_out, stats_out, max_stats);
     if (n_rounds_out) *n_rounds_out = r;
   });
 }
@@ -147,17 +149,29 @@ rp_status rp_rollout_tail_batched(rp_engine* eng, int32_t n_prompts, int32_t r_s
                                   const int32_t* prompt_tokens, const int64_t* prompt_offsets,
                                   const int32_t* max_new_tokens, uint64_t seed, float temperature, int32_t P0,
                                   int32_t R0, float eta_p, float eta_r, int32_t* resp_tokens_out,
-                                  int32_t* resp_len_out,
-                                  int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats_out,
-                                  int32_t max_stats, int32_t* n_rounds_out) {
+                                  float* resp_logprobs_out, int32_t* resp_len_out, int32_t* accept_round_out,
+                                  int32_t* kept_out, rp_round_stats* stats_out, int32_t max_stats,
+                                  int32_t* n_rounds_out) {
   return engine_call(eng, [&](rollpack::Engine* e) {
     if (max_stats < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "max_stats must be >= 0");
     const int32_t r = e->rollout_tail_batched(n_prompts, r_spec, seq_ids, prompt_tokens, prompt_offsets,
                                               max_new_tokens, seed, temperature, P0, R0, eta_p, eta_r,
-                                              resp_tokens_out,
-                                              resp_len_out, accept_round_out, kept_out, stats_out, max_stats);
+                                              resp_tokens_out, resp_logprobs_out, resp_len_out, accept_round_out,
+                                              kept_out, stats_out, max_stats);
     if (n_rounds_out) *n_rounds_out = r;
   });
+}
+
+rp_status rp_get_logprobs(rp_engine* eng, int64_t seq_id, float* out, int32_t cap, int32_t* len_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    if (cap < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "cap must be >= 0");
+    const int32_t k = e->get_logprobs(seq_id, out, cap);
+    if (len_out) *len_out = k;
+  });
+}
+
+rp_status rp_set_eos(rp_engine* eng, int32_t eos_token) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->set_eos(eos_token); });
 }
 
 rp_status rp_plan_tail_batching(int32_t n_prompts, int32_t r_spec, const int32_t* lens, int32_t P0, int32_t R0,

@@ -96,12 +96,14 @@ SIGNATURES = {
     "rp_free_finished": (ctypes.c_int, [_P, _I64P, ctypes.c_int32, _I32P]),
     "rp_abort": (ctypes.c_int, [_P, ctypes.c_int32, _I64P]),
     "rp_get_tokens": (ctypes.c_int, [_P, ctypes.c_int64, _I32P, ctypes.c_int32, _I32P]),
+    "rp_get_logprobs": (ctypes.c_int, [_P, ctypes.c_int64, _F32P, ctypes.c_int32, _I32P]),
+    "rp_set_eos": (ctypes.c_int, [_P, ctypes.c_int32]),
     "rp_rollout_generate": (ctypes.c_int, [_P, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P, ctypes.c_uint64,
-                                           ctypes.c_float, _I32P, _I32P, ctypes.POINTER(RpRoundStats),
+                                           ctypes.c_float, _I32P, _I32P, _F32P, _I32P, ctypes.POINTER(RpRoundStats),
                                            ctypes.c_int32, _I32P]),
     "rp_rollout_tail_batched": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P,
                                                ctypes.c_uint64, ctypes.c_float, ctypes.c_int32, ctypes.c_int32,
-                                               ctypes.c_float, ctypes.c_float, _I32P, _I32P, _I32P, _I32P,
+                                               ctypes.c_float, ctypes.c_float, _I32P, _F32P, _I32P, _I32P, _I32P,
                                                ctypes.POINTER(RpRoundStats), ctypes.c_int32, _I32P]),
     "rp_plan_tail_batching": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_int32, ctypes.c_int32,
                                              ctypes.c_float, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, _I32P, _I32P, _I32P,
@@ -216,28 +218,46 @@ def rp_get_tokens(eng: int, seq_id: int, cap: int) -> np.ndarray:
 
 
 def rp_rollout_generate(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed: int,
-                        temperature: float, round_ids=None, max_stats: int = 16):
+                        temperature: float, round_ids=None, max_stats: int = 16, details: bool = False):
+    """Returns (tokens, stats); with details=True (tokens, logprobs, lengths, stats)."""
     ids, ids_p = _arr(seq_ids, np.int64)
     toks, toks_p = _arr(prompt_tokens, np.int32)
     offs, offs_p = _arr(prompt_offsets, np.int64)
     mn, mn_p = _arr(max_new_tokens, np.int32)
     rid, rid_p = _opt(round_ids, np.int32)
     resp = np.zeros(int(mn.sum()), np.int32)
+    logp = np.zeros(int(mn.sum()), np.float32) if details else None
+    lens = np.zeros(len(ids), np.int32) if details else None
     stats = (RpRoundStats * max_stats)()
     nr = ctypes.c_int32()
     _check(load_library().rp_rollout_generate(eng, len(ids), ids_p, toks_p, offs_p, mn_p, ctypes.c_uint64(seed),
-                                              ctypes.c_float(temperature), rid_p, resp.ctypes.data_as(_I32P), stats,
+                                              ctypes.c_float(temperature), rid_p, resp.ctypes.data_as(_I32P),
+                                              None if logp is None else logp.ctypes.data_as(_F32P),
+                                              None if lens is None else lens.ctypes.data_as(_I32P), stats,
                                               max_stats, ctypes.byref(nr)))
-    return resp, [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
+    st = [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
+    return (resp, logp, lens, st) if details else (resp, st)
+
+
+def rp_get_logprobs(eng: int, seq_id: int, cap: int) -> np.ndarray:
+    out = np.zeros(max(cap, 1), np.float32)
+    n = ctypes.c_int32()
+    _check(load_library().rp_get_logprobs(eng, seq_id, out.ctypes.data_as(_F32P), cap, ctypes.byref(n)))
+    return out[:min(n.value, cap)]
+
+
+def rp_set_eos(eng: int, eos_token: int) -> None:
+    _check(load_library().rp_set_eos(eng, eos_token))
 
 
 def rp_rollout_tail_batched(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed: int,
                             temperature: float, P0: int, R0: int, eta: float, eta_r: Optional[float] = None,
-                            max_stats: int = 0):
+                            max_stats: int = 0, logprobs: bool = False):
     """seq_ids, max_new_tokens: [n_prompts, r_spec]; prompt CSR over prompts.  eta is the prompt
     speculation factor and, unless eta_r is given, the response factor too.
 
-    Returns (resp_tokens, resp_len [n, r_spec], accept_round [n], kept [n, r_spec] bool, round stats)."""
+    Returns (resp_tokens, resp_len [n, r_spec], accept_round [n], kept [n, r_spec] bool, round stats),
+    and the log-probabilities last when logprobs=True."""
     ids = np.ascontiguousarray(seq_ids, np.int64)
     n, r_spec = ids.shape
     toks, toks_p = _arr(prompt_tokens, np.int32)
@@ -246,6 +266,7 @@ def rp_rollout_tail_batched(eng: int, seq_ids, prompt_tokens, prompt_offsets, ma
     assert mn.shape == ids.shape and len(offs) == n + 1
     max_stats = max_stats or 2 * n + 2
     resp = np.zeros(max(int(mn.sum()), 1), np.int32)
+    logp = np.zeros(max(int(mn.sum()), 1), np.float32) if logprobs else None
     glen = np.zeros((n, r_spec), np.int32)
     acc = np.zeros(n, np.int32)
     kept = np.zeros((n, r_spec), np.int32)
@@ -255,9 +276,10 @@ def rp_rollout_tail_batched(eng: int, seq_ids, prompt_tokens, prompt_offsets, ma
     _check(load_library().rp_rollout_tail_batched(eng, n, r_spec, ids.ctypes.data_as(_I64P), toks_p, offs_p, P(mn),
                                                   ctypes.c_uint64(seed), ctypes.c_float(temperature), P0, R0,
                                                   ctypes.c_float(eta), ctypes.c_float(eta if eta_r is None else eta_r),
-                                                  P(resp), P(glen), P(acc), P(kept), stats,
-                                                  max_stats, ctypes.byref(nr)))
-    return resp, glen, acc, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
+                                                  P(resp), None if logp is None else logp.ctypes.data_as(_F32P),
+                                                  P(glen), P(acc), P(kept), stats, max_stats, ctypes.byref(nr)))
+    out = (resp, glen, acc, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))])
+    return out + (logp,) if logprobs else out
 
 
 def rp_plan_tail_batching(lens, P0: int, R0: int, eta: float, eta_r: Optional[float] = None):
@@ -405,6 +427,12 @@ class Engine:
     def get_tokens(self, seq_id: int, cap: int):
         return rp_get_tokens(self.handle, seq_id, cap)
 
+    def get_logprobs(self, seq_id: int, cap: int):
+        return rp_get_logprobs(self.handle, seq_id, cap)
+
+    def set_eos(self, eos_token: int):
+        rp_set_eos(self.handle, eos_token)
+
     def set_kv_policy(self, policy: int):
         rp_set_kv_policy(self.handle, policy)
 
@@ -417,9 +445,10 @@ class Engine:
     def profile_read(self):
         return rp_profile_read(self.handle)
 
-    def rollout(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature, round_ids=None):
+    def rollout(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature, round_ids=None,
+                details: bool = False):
         return rp_rollout_generate(self.handle, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
-                                   temperature, round_ids)
+                                   temperature, round_ids, details=details)
 
 
     def rollout_tail_batched(self, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,

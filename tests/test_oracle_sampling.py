@@ -79,3 +79,33 @@ def test_greedy_and_ties():
     # a very low temperature concentrates on the argmax
     l2 = np.array([0.0, 5.0, 1.0])
     assert all(osm.sample(l2, 0.01, 3, 4, p) == 1 for p in range(50))
+
+
+def test_logprob_closed_forms():
+    V = 151936
+    assert osm.logprob(np.zeros(V), 1.0, 17) == pytest.approx(-np.log(V), abs=1e-12)   # uniform
+    a, b = 2.5, -1.0                                                                     # two tokens: log sigmoid
+    assert osm.logprob(np.array([a, b]), 1.0, 0) == pytest.approx(-np.log1p(np.exp(b - a)), abs=1e-14)
+    assert osm.logprob(np.array([a, b]), 0.5, 1) == pytest.approx(-np.log1p(np.exp((a - b) / 0.5)), abs=1e-12)
+    big = np.full(1000, -1e4)
+    big[3] = 1e4                                                                         # no overflow, p -> 1
+    assert osm.logprob(big, 1.0, 3) == pytest.approx(0.0, abs=1e-12)
+    assert osm.logprob(big, 1.0, 4) == pytest.approx(-2e4, rel=1e-12)
+
+
+def test_logprob_invariants():
+    rng = np.random.default_rng(4)
+    l = rng.standard_normal(300) * 3
+    for T in (0.0, 0.7, 1.0, 1.6):
+        lp = np.array([osm.logprob(l, T, v) for v in range(300)])
+        assert np.exp(lp).sum() == pytest.approx(1.0, abs=1e-12)                       # a distribution
+        assert osm.logprob(l + 123.0, T, 7) == pytest.approx(lp[7], abs=1e-12)         # shift invariance
+        t = 1.0 if T == 0 else T
+        assert osm.logprob(l / t, 1.0, 11) == pytest.approx(lp[11], abs=1e-12)          # temperature = rescaled logits
+        assert np.argmax(lp) == np.argmax(l)                                            # monotone in the logit
+
+
+def test_stop_at_eos():
+    assert osm.stop_at([5, 9, 3, 9, 1], 9) == [5, 9]
+    assert osm.stop_at([5, 9, 3], 4) == [5, 9, 3]
+    assert osm.stop_at([4], 4) == [4]
