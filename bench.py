@@ -141,6 +141,9 @@ def main():
     ap.add_argument("--kernel", default="gemm_gate_up", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--max-prefill-tokens", type=int, default=16384)
+    ap.add_argument("--step-trace", default=None, metavar="PATH",
+                    help="after the timed steps, run one more (untimed) round with the per-step trace on and write "
+                         "its records (kind, round, rows, summed context, ms) to PATH as JSON")
     ap.add_argument("--compare-unscheduled", action="store_true",
                     help="after the timed steps, run the same sequences as one unscheduled batch and report "
                          "both schedules (meaningful for 7b-mixed: short round + long round vs one batch)")
@@ -243,6 +246,18 @@ def main():
             "unscheduled_idle_slot_s": round(flat[0]["idle_slot_s"], 1),
             "unscheduled_slot_idle": round(flat[0]["slot_idle"], 4),
             "idle_reduction": round(flat[0]["idle_slot_s"] / max(sched_idle, 1e-9), 3)}
+    if args.step_trace:
+        log("running one more round with the per-step trace")
+        eng.step_trace(1 << 20)
+        call()
+        rec = eng.step_trace_read()
+        eng.step_trace(0)
+        with open(args.step_trace, "w") as f:
+            json.dump({"workload": args.workload, "model": shape.name, "fields": ["kind", "round_id", "rows",
+                                                                                 "sum_ctx", "ms"],
+                       "records": [[int(r["kind"]), int(r["round_id"]), int(r["rows"]), int(r["sum_ctx"]),
+                                    round(float(r["ms"]), 5)] for r in rec]}, f)
+        log(f"step trace: {len(rec)} records written to {args.step_trace}")
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(weights, shape, wl)

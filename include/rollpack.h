@@ -380,6 +380,31 @@ rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask);
  * record per (class, phase) with launches > 0, into host out [cap]. */
 rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int32_t* n_out);
 
+/* One step of the engine: a decode step over `rows` sequences with
+ * `sum_ctx` context tokens in total, or one prefill chunk of `rows` tokens
+ * (sum_ctx then counts the keys its queries attend to).  ms is the HIP-event
+ * time from the step's first launch to its sampler's end on the engine's
+ * stream; round_id is the round of rp_rollout_generate /
+ * rp_rollout_tail_batched that ran it (-1 outside a rollout call). */
+typedef struct rp_step_record {
+  int32_t kind;      /* 0 decode step, 1 prefill chunk */
+  int32_t round_id;
+  int32_t rows;
+  int32_t reserved;
+  int64_t sum_ctx;
+  double ms;
+} rp_step_record;
+
+/* Per-step trace, the measurement behind the paper's step-time profiles
+ * (section 4.1) and the round metrics: from now on record up to `cap` steps
+ * (0 stops and discards the trace).  Two HIP events bracket each step. */
+rp_status rp_step_trace_enable(rp_engine* eng, int32_t cap);
+
+/* Synchronise, then copy the recorded steps to host out [cap] in order and
+ * clear the trace; n_out gets the number copied (steps beyond the enabled
+ * capacity are not recorded). */
+rp_status rp_step_trace_read(rp_engine* eng, rp_step_record* out, int32_t cap, int32_t* n_out);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* rp_last_error(void);
 

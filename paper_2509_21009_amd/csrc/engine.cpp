@@ -202,6 +202,63 @@ Engine::~Engine() {
     (void)hipHostFree(c.host);
     (void)hipEventDestroy(c.ev);
   }
+  for (auto& t : trace_) {
+    (void)hipEventDestroy(t.e0);
+    (void)hipEventDestroy(t.e1);
+  }
+  for (auto e : trace_pool_) (void)hipEventDestroy(e);
+}
+
+Engine::TraceRec* Engine::trace_begin(int kind, int rows, int64_t sum_ctx) {
+  if (static_cast<int32_t>(trace_.size()) >= trace_cap_) return nullptr;
+  auto take = [&]() {
+    hipEvent_t e;
+    if (!trace_pool_.empty()) {
+      e = trace_pool_.back();
+      trace_pool_.pop_back();
+    } else {
+      HIP_TRY(hipEventCreate(&e));
+    }
+    return e;
+  };
+  TraceRec t{rp_step_record{kind, cur_round_, rows, 0, sum_ctx, 0.0}, take(), take()};
+  HIP_TRY(hipEventRecord(t.e0, stream_));
+  trace_.push_back(t);
+  return &trace_.back();
+}
+
+void Engine::trace_end(TraceRec* t) {
+  if (t) HIP_TRY(hipEventRecord(t->e1, stream_));
+}
+
+void Engine::step_trace_enable(int32_t cap) {
+  if (cap < 0) throw RpError(RP_ERR_INVALID_ARG, "trace capacity must be >= 0");
+  HIP_TRY(hipStreamSynchronize(stream_));
+  for (auto& t : trace_) {
+    trace_pool_.push_back(t.e0);
+    trace_pool_.push_back(t.e1);
+  }
+  trace_.clear();
+  trace_.reserve(static_cast<size_t>(cap));  // pointers handed out by trace_begin stay valid
+  trace_cap_ = cap;
+}
+
+int32_t Engine::step_trace_read(rp_step_record* out, int32_t cap) {
+  if (cap < 0 || (cap > 0 && !out)) throw RpError(RP_ERR_INVALID_ARG, "step_trace_read: bad output");
+  HIP_TRY(hipStreamSynchronize(stream_));
+  const int32_t n = std::min<int32_t>(cap, static_cast<int32_t>(trace_.size()));
+  for (int32_t i = 0; i < n; ++i) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, trace_[i].e0, trace_[i].e1));
+    out[i] = trace_[i].rec;
+    out[i].ms = ms;
+  }
+  for (auto& t : trace_) {
+    trace_pool_.push_back(t.e0);
+    trace_pool_.push_back(t.e1);
+  }
+  trace_.clear();
+  return n;
 }
 
 void Engine::set_eos(int32_t token) {
@@ -539,7 +596,9 @@ void Engine::run_prefill_chunk(const std::vector<PrefillPiece>& pcs, float* logi
   m_seq_slot_ = d + 3 * T; m_seq_row0_ = m_seq_slot_ + n; m_seq_pos0_ = m_seq_row0_ + n;
   m_seq_ntok_ = m_seq_pos0_ + n; m_item_off_ = m_seq_ntok_ + n; m_last_row_ = m_item_off_ + n + 1;
   m_gen_pos_ = m_last_row_ + n; m_gen_hist_ = m_gen_pos_ + n; m_gen_slot_ = m_seq_slot_;
+  TraceRec* tr = trace_cap_ ? trace_begin(1, T, static_cast<int64_t>(sum_ctx_sq_ / 2)) : nullptr;
   forward(T, true, n, items, 0, 0);
+  trace_end(tr);
   std::vector<std::array<int64_t, 3>> sampled;  // pieces that end their sequence sampled its next token
   for (const PrefillPiece& pc : pcs)
     if (pc.seq >= 0) sampled.push_back({pc.slot, slots_[pc.slot].id, pc.hist0});
@@ -731,7 +790,9 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
   m_in_tok_ = d; m_slot_ = d + B; m_pos_ = d + 2 * B; m_ctx_ = d + 3 * B; m_split_off_ = d + 4 * B;
   m_gen_pos_ = d + 5 * B + 1; m_gen_hist_ = d + 6 * B + 1; m_gen_slot_ = m_slot_;
   m_split_desc_ = d + desc_at;
+  TraceRec* tr = trace_cap_ ? trace_begin(0, B, sum_ctx_) : nullptr;
   forward(B, false, 0, 0, total_splits, tps);
+  trace_end(tr);
   if (logits_out) {
     HIP_TRY(hipMemcpyAsync(logits_out, scratch_ + plan_.logits, static_cast<size_t>(B) * cfg_.vocab * 4,
                            hipMemcpyDeviceToDevice, stream_));
@@ -1226,7 +1287,9 @@ int32_t Engine::rollout(int32_t n, const int64_t* ids, const int32_t* toks, cons
   for (auto& kv : rounds) {
     rp_round_stats st{};
     st.round_id = kv.first;
+    cur_round_ = kv.first;
     run_round(kv.second, arr, resp_out, len_out, nullptr, &st);
+    cur_round_ = -1;
     if (stats && r_idx < max_stats) stats[r_idx] = st;
     ++r_idx;
   }
@@ -1289,6 +1352,7 @@ int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const in
   while (next_fresh < n_prompts || !queue.empty()) {
     rp_round_stats st{};
     st.round_id = k;
+    cur_round_ = k;
     std::vector<int32_t> launched, members;
     if (static_cast<int32_t>(queue.size()) >= P0 || (next_fresh >= n_prompts && !queue.empty())) {
       // Long round: the oldest queued prompts, R0 responses each, no speculation.
@@ -1329,6 +1393,7 @@ int32_t Engine::rollout_tail_batched(int32_t n_prompts, int32_t r_spec, const in
         }
       }
     }
+    cur_round_ = -1;
     if (stats && k < max_stats) stats[k] = st;
     ++k;
   }

@@ -136,6 +136,8 @@ class Engine {
   void profile_enable(uint32_t mask);
   int32_t profile_read(rp_kernel_stats* out, int32_t cap);
   void set_kv_policy(int32_t policy);
+  void step_trace_enable(int32_t cap);
+  int32_t step_trace_read(rp_step_record* out, int32_t cap);
   void kv_status(int64_t* free_pages, int32_t* running, int32_t* waiting, int64_t* preemptions,
                  int64_t* recomputed_tokens) const;
 
@@ -215,6 +217,17 @@ class Engine {
     int32_t* host;  // pinned copy of tokens_cur
     std::vector<std::array<int64_t, 3>> rows;
   };
+  // per-step trace (rp_step_trace_*)
+  struct TraceRec {
+    rp_step_record rec;
+    hipEvent_t e0, e1;
+  };
+  std::vector<TraceRec> trace_;
+  std::vector<hipEvent_t> trace_pool_;
+  int32_t trace_cap_ = 0;
+  int32_t cur_round_ = -1;
+  TraceRec* trace_begin(int kind, int rows, int64_t sum_ctx);
+  void trace_end(TraceRec* t);
   int32_t eos_token_ = -1;
   int64_t sample_step_ = 0;   // sampler launches so far
   int64_t eos_applied_ = -1;  // every sample step up to this one has been checked

@@ -223,6 +223,17 @@ rp_status rp_kv_status(rp_engine* eng, int64_t* free_pages, int32_t* running, in
   });
 }
 
+rp_status rp_step_trace_enable(rp_engine* eng, int32_t cap) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->step_trace_enable(cap); });
+}
+
+rp_status rp_step_trace_read(rp_engine* eng, rp_step_record* out, int32_t cap, int32_t* n_out) {
+  return engine_call(eng, [&](rollpack::Engine* e) {
+    const int32_t n = e->step_trace_read(out, cap);
+    if (n_out) *n_out = n;
+  });
+}
+
 rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask) {
   return engine_call(eng, [&](rollpack::Engine* e) { e->profile_enable(class_mask); });
 }

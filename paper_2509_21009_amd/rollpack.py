@@ -70,6 +70,11 @@ class RpKernelStats(ctypes.Structure):
                 "launches": self.launches, "total_ms": self.total_ms, "bytes": self.bytes, "flops": self.flops}
 
 
+class RpStepRecord(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("round_id", ctypes.c_int32), ("rows", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("sum_ctx", ctypes.c_int64), ("ms", ctypes.c_double)]
+
+
 class RollpackError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{STATUS.get(status, status)}: {msg}")
@@ -110,6 +115,8 @@ SIGNATURES = {
                                              _I32P, _I32P, _I32P, _I32P, _I32P]),
     "rp_set_kv_policy": (ctypes.c_int, [_P, ctypes.c_int32]),
     "rp_kv_status": (ctypes.c_int, [_P, _I64P, _I32P, _I32P, _I64P, _I64P]),
+    "rp_step_trace_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "rp_step_trace_read": (ctypes.c_int, [_P, ctypes.POINTER(RpStepRecord), ctypes.c_int32, _I32P]),
     "rp_profile_enable": (ctypes.c_int, [_P, ctypes.c_uint32]),
     "rp_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(RpKernelStats), ctypes.c_int32, _I32P]),
     "rp_last_error": (ctypes.c_char_p, []),
@@ -327,6 +334,23 @@ def rp_kv_status(eng: int) -> dict:
             "recomputed_tokens": rt.value}
 
 
+def rp_step_trace_enable(eng: int, cap: int) -> None:
+    _check(load_library().rp_step_trace_enable(eng, cap))
+
+
+def rp_step_trace_read(eng: int, cap: int) -> np.ndarray:
+    """Structured array of the recorded steps: kind, round_id, rows, sum_ctx, ms."""
+    out = (RpStepRecord * max(cap, 1))()
+    n = ctypes.c_int32()
+    _check(load_library().rp_step_trace_read(eng, out, cap, ctypes.byref(n)))
+    rec = np.zeros(n.value, dtype=[("kind", np.int32), ("round_id", np.int32), ("rows", np.int32),
+                                   ("sum_ctx", np.int64), ("ms", np.float64)])
+    for i in range(n.value):
+        r = out[i]
+        rec[i] = (r.kind, r.round_id, r.rows, r.sum_ctx, r.ms)
+    return rec
+
+
 def rp_profile_enable(eng: int, classes) -> None:
     """classes: iterable of names from KERNEL_CLASSES (empty stops profiling)."""
     mask = 0
@@ -438,6 +462,12 @@ class Engine:
 
     def kv_status(self) -> dict:
         return rp_kv_status(self.handle)
+
+    def step_trace(self, cap: int):
+        rp_step_trace_enable(self.handle, cap)
+
+    def step_trace_read(self, cap: int = 1 << 20):
+        return rp_step_trace_read(self.handle, cap)
 
     def profile(self, classes):
         rp_profile_enable(self.handle, classes)

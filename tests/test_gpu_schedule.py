@@ -132,3 +132,27 @@ def test_short_round_that_cannot_start_at_once_is_rejected(tiny):
                                                             1.0)
     eng.close()
     assert kept.all() and len(stats) == 2
+
+
+def test_step_trace_records_every_step(tiny):
+    """rp_step_trace_*: one record per prefill chunk and decode step, with rows, context sums and round ids."""
+    s, wd = tiny
+    from workloads import make_workload
+    wl = make_workload("tiny")
+    mn = np.array([5, 64, 1, 30, 64, 2, 17, 40], np.int32)
+    eng = _engine(s, wd, max_seqs=8, pages=32)
+    eng.step_trace(1000)
+    _, st = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, mn, 3, 1.0,
+                        np.array([4, 4, 4, 4, 9, 9, 9, 9], np.int32))
+    rec = eng.step_trace_read()
+    eng.step_trace(0)
+    eng.close()
+    dec = rec[rec["kind"] == 0]
+    assert len(dec) == sum(x["decode_steps"] for x in st) and (rec["kind"] == 1).sum() == 2
+    assert set(rec["round_id"].tolist()) == {4, 9} and (rec["ms"] > 0).all()
+    # decode rows: live sequences per step of each round (all admitted together, one token per step)
+    for rid, lens in ((4, mn[:4]), (9, mn[4:])):
+        rows = dec[dec["round_id"] == rid]["rows"].tolist()
+        assert rows == [int((lens > j).sum()) for j in range(1, int(lens.max()))]
+        ctx = dec[dec["round_id"] == rid]["sum_ctx"].tolist()
+        assert ctx == [int(sum(32 + j for L in lens if L > j)) for j in range(1, int(lens.max()))]
