@@ -20,9 +20,9 @@
 //    unchanged).  The 4 waves of a block split the chunk range and reduce
 //    through LDS; blockIdx.y splits K further and writes fp32 partials that
 //    the consumer kernel sums.
-//  * k_gemm_tiled (M > 64: prefill and large decode batches): 128x128 block
-//    tiles staged through padded LDS, 2x2 waves of 64x64, register prefetch
-//    of the next K block.
+//  * k_gemm_tiled (M > 64: prefill and large decode batches): 128- or
+//    256-row x 256 block tiles, 2x4 waves of 32x32x16 MFMAs, tiles loaded
+//    from global memory straight into a 4-stage swizzled LDS ring.
 //  * k_gemm_f32: fp32 FMA tiles for the fp32 model (no reduced precision).
 //
 // The SiLU epilogue pairs gate row i with up row i in one thread and writes
@@ -448,29 +448,64 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
 }
 
 // ---- prefill / large-batch tiled MFMA GEMM ---------------------------------
-// Block tile: 256 activation rows (m) x 256 weight rows (n), K step 64, eight
-// waves as 2 (m) x 4 (n), each computing 128 m x 64 n with
-// v_mfma_f32_32x32x16_bf16 (4 x 2 tiles, 128 fp32 accumulators per lane; two
-// waves per SIMD).  Activations are the MFMA row operand and weights the
-// column operand, so the 32 lanes of one accumulator register hold 32
-// consecutive n: coalesced stores.  Tiles move HBM -> registers -> padded
-// LDS (two stages); the next K step is loaded into registers while the
-// current one is multiplied, one barrier per K step, and each wave
-// double-buffers its LDS fragments across the four 16-wide MFMA k-steps.
-// Global loads go through buffer resources: a wave's 8-row slab of a weight
-// tile lies in one weight segment, and rows past M or N read as zeros.
-// Tiles are ordered so that the blocks an XCD runs back to back (ids equal
-// mod 8) walk the m tiles of one weight panel, which then stays in that
-// XCD's L2.
-constexpr int kGBM = 256, kGBN = 256, kGBK = 64, kGLD = kGBK + 8;
+// Block tile: BM activation rows (m, 128 or 256) x 256 weight rows (n), K step
+// 32, eight waves as 2 (m) x 4 (n), each computing BM/2 m x 64 n with
+// v_mfma_f32_32x32x16_bf16 (two waves per SIMD).  Activations are the MFMA
+// row operand and weights the column operand, so the 32 lanes of one
+// accumulator register hold 32 consecutive n: coalesced stores.
+//
+// Tiles move from global memory straight into LDS (buffer_load_dwordx4 ...
+// lds: each wave-instruction writes 1 KB, 16 rows of 64 bytes, with no
+// register staging) through a ring of kGNST stages, issued kGNST - 1 stages
+// ahead, one barrier per K step.  The loads are inline assembly, so the
+// compiler neither tracks them nor inserts its conservative vmcnt(0) before
+// every barrier; the kernel waits with explicit vmcnt counts instead (each
+// thread issues the same NA + 2 loads per stage, and vector loads complete in
+// order).  A stage's buffer is refilled only after the barrier that follows
+// the last read of it.  The 16-byte chunk j of LDS row r holds global chunk
+// j ^ ((r >> 2) & 3): eight consecutive lanes of a fragment read then hit
+// eight distinct 16-byte bank groups.  Rows past M or N read as zeros
+// through the buffer resources (range-checked loads); a 16-row block of a
+// weight tile lies in one weight segment.  Tiles are ordered so that the
+// blocks an XCD runs back to back (ids equal mod 8) walk the m tiles of one
+// weight panel, which then stays in that XCD's L2.
+constexpr int kGBN = 256, kGBK = 32, kGNST = 4;
 
-template <bool SILU>
+typedef uint32_t u32x4_raw __attribute__((ext_vector_type(4)));
+// Buffer descriptor with the same fields as buffer_rsrc (base, stride 0, size, flags), as the
+// four raw dwords an inline-assembly operand needs.
+__device__ __forceinline__ u32x4_raw raw_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t addr = reinterpret_cast<uint64_t>(p);
+  return u32x4_raw{static_cast<uint32_t>(addr), static_cast<uint32_t>(addr >> 32) & 0xffffu, bytes, 0x00020000u};
+}
+// 16 bytes per lane from byte voff of the buffer into LDS at lds + 16 * lane (M0 holds the base).
+__device__ __forceinline__ void dma16(u32x4_raw r, uint32_t lds, int voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "s"(lds), "v"(voff), "s"(r) : "memory");
+}
+// s_waitcnt vmcnt(N), the other counters at their maxima (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// Wait until at most PER * min(after, MAXJ) loads are outstanding.
+template <int PER, int J, int MAXJ>
+__device__ __forceinline__ void wait_stages_after(int after) {
+  if constexpr (J >= MAXJ) {
+    wait_vmcnt<PER * MAXJ>();
+  } else {
+    if (after == J) wait_vmcnt<PER * J>();
+    else wait_stages_after<PER, J + 1, MAXJ>(after);
+  }
+}
+__device__ __forceinline__ int gswz(int r) { return (r >> 2) & 3; }
+
+template <int BM, bool SILU>
 __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_split, int n_mb, int n_nb) {
-  // one LDS array: stage st of the activation tile at st * kGBM * kGLD, of the weight tile
-  // after both activation stages (two separate arrays cost registers for their bases)
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (kGBM + kGBN) * kGLD];
-  bf16_t* const As = smem;
-  bf16_t* const Ws = smem + 2 * kGBM * kGLD;
+  constexpr int STAGE = (BM + kGBN) * kGBK;  // elements per stage
+  constexpr int MT = BM / 64;                // 32-row activation tiles per wave
+  constexpr int NA = BM / 128;               // 16-row activation blocks a wave loads per stage
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[kGNST * STAGE];
   const int n_tiles = n_mb * n_nb;
   const int per_xcd = (n_tiles + 7) / 8;
   const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
@@ -483,15 +518,20 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
   const int l32 = lane & 31, lh = lane >> 5;
   const int K = a.K;
 
-  // global -> LDS staging: thread rows (tid >> 3) + 64 i, 16-byte column piece (tid & 7)
-  const int trow = tid >> 3, tcol = (tid & 7) * 8;
-  const __amdgpu_buffer_rsrc_t ars = buffer_rsrc(a.A, static_cast<uint32_t>(a.M) * static_cast<uint32_t>(a.lda) * 2u);
-  int aoff[4], woff[4];
-  __amdgpu_buffer_rsrc_t wrs[4];
+  // Loads: wave w fills 16-row blocks w + 8 i of each tile; lane -> row lane >> 2 of the block,
+  // LDS chunk lane & 3, which holds global chunk (lane & 3) ^ gswz(row).
+  const u32x4_raw ars = raw_rsrc(a.A, static_cast<uint32_t>(a.M) * static_cast<uint32_t>(a.lda) * 2u);
+  int aoff[NA], woff[2];
+  u32x4_raw wrs[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    aoff[i] = ((mb * kGBM + trow + 64 * i) * static_cast<int>(a.lda) + tcol) * 2;
-    const int r0 = wave * 8 + 64 * i;  // the wave's 8-row slab of the weight tile
+  for (int i = 0; i < NA; ++i) {
+    const int r = (wave + 8 * i) * 16 + (lane >> 2);
+    aoff[i] = ((mb * BM + r) * static_cast<int>(a.lda) + ((lane & 3) ^ gswz(r)) * 8) * 2;
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r0 = (wave + 8 * i) * 16;
+    const int r = r0 + (lane >> 2);
     const bf16_t* wb;
     int rel0, rows_valid;
     if (SILU) {  // 32-row groups alternate gate / up over the same output indices
@@ -507,12 +547,15 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
       rel0 = n0 - b;
       rows_valid = n0 < a.N ? a.W.rows[sg] : 0;
     }
-    wrs[i] = buffer_rsrc(wb, static_cast<uint32_t>(rows_valid) * static_cast<uint32_t>(K) * 2u);
-    woff[i] = ((rel0 + (trow & 7)) * K + tcol) * 2;
+    wrs[i] = raw_rsrc(wb, static_cast<uint32_t>(rows_valid) * static_cast<uint32_t>(K) * 2u);
+    woff[i] = ((rel0 + (lane >> 2)) * K + ((lane & 3) ^ gswz(r)) * 8) * 2;
   }
-  f32x16_t acc[4][2];
+  typedef const __attribute__((address_space(3))) char lds_char;
+  const uint32_t lds0 = static_cast<uint32_t>((uintptr_t)(lds_char*)(smem));
+
+  f32x16_t acc[MT][2];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
@@ -520,79 +563,77 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
 
   const int kb0 = split * kblocks_per_split;
   const int kb1 = min(kb0 + kblocks_per_split, K / kGBK);
-  bf16x8_t ra[4], rw[4];
-  auto load = [&](int kb) {
+  auto load = [&](int st, int kb) {
     const int ko = kb * kGBK * 2;
+    const uint32_t sa = lds0 + static_cast<uint32_t>(st * STAGE * 2), sw = sa + BM * kGBK * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ra[i] = load_bf16x8(ars, aoff[i] + ko);
+    for (int i = 0; i < NA; ++i)
+      dma16(ars, __builtin_amdgcn_readfirstlane(sa + static_cast<uint32_t>((wave + 8 * i) * 1024)), aoff[i] + ko);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) rw[i] = load_bf16x8(wrs[i], woff[i] + ko);
-  };
-  auto store = [&](int st) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = trow + 64 * i;
-      *reinterpret_cast<bf16x8_t*>(&As[st * kGBM * kGLD + row * kGLD + tcol]) = ra[i];
-      *reinterpret_cast<bf16x8_t*>(&Ws[st * kGBN * kGLD + row * kGLD + tcol]) = rw[i];
-    }
+    for (int i = 0; i < 2; ++i)
+      dma16(wrs[i], __builtin_amdgcn_readfirstlane(sw + static_cast<uint32_t>((wave + 8 * i) * 1024)), woff[i] + ko);
   };
   auto compute = [&](int st) {
-    const bf16_t* as = As + st * kGBM * kGLD + (wm * 128 + l32) * kGLD + 8 * lh;
-    const bf16_t* ws = Ws + st * kGBN * kGLD + (wn * 64 + l32) * kGLD + 8 * lh;
-    bf16x8_t af[2][4], bw[2][2];
-    auto rd = [&](int buf, int kk) {
+    const bf16_t* sA = smem + st * STAGE;
+    const bf16_t* sW = sA + BM * kGBK;
+    bf16x8_t af[2][MT], bw[2][2];
+    auto rd = [&](int buf, int ki) {
+      const int c = ki * 2 + lh;  // the lane's 16-byte chunk of this k-step
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) af[buf][mt] = load_bf16x8(as + mt * 32 * kGLD + kk);
+      for (int mt = 0; mt < MT; ++mt) {
+        const int r = wm * (BM / 2) + mt * 32 + l32;
+        af[buf][mt] = *reinterpret_cast<const bf16x8_t*>(sA + r * kGBK + (c ^ gswz(r)) * 8);
+      }
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) bw[buf][nt] = load_bf16x8(ws + nt * 32 * kGLD + kk);
+      for (int nt = 0; nt < 2; ++nt) {
+        const int r = wn * 64 + nt * 32 + l32;
+        bw[buf][nt] = *reinterpret_cast<const bf16x8_t*>(sW + r * kGBK + (c ^ gswz(r)) * 8);
+      }
     };
-    // The next k-step's fragment reads are interleaved one-for-one with this
-    // k-step's MFMAs, at raised wave priority, so that the SIMD's other wave
-    // (in the same phase) finds MFMA issue slots between them.
+    // The second k-step's fragment reads are interleaved with the first k-step's MFMAs, at
+    // raised wave priority, so that the SIMD's other wave finds MFMA issue slots between them.
     rd(0, 0);
 #pragma unroll
     for (int ki = 0; ki < kGBK / 16; ++ki) {
       __builtin_amdgcn_s_setprio(1);
-      if (ki + 1 < kGBK / 16) rd((ki + 1) & 1, (ki + 1) * 16);
+      if (ki + 1 < kGBK / 16) rd((ki + 1) & 1, ki + 1);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma32x32x16(af[ki & 1][mt], bw[ki & 1][nt], acc[mt][nt]);
       if (ki + 1 < kGBK / 16) {
 #pragma unroll
-        for (int q = 0; q < 6; ++q) {
+        for (int q = 0; q < MT + 2; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        if constexpr (MT > 2) __builtin_amdgcn_sched_group_barrier(0x008, MT - 2, 0);
       }
       __builtin_amdgcn_s_setprio(0);
     }
   };
-  if (kb0 < kb1) {
-    load(kb0);
-    store(0);
-    if (kb0 + 1 < kb1) load(kb0 + 1);
-  }
-  __syncthreads();
-  for (int kb = kb0; kb < kb1; kb += 2) {
-    compute(0);
-    if (kb + 1 < kb1) store(1);
-    if (kb + 2 < kb1) load(kb + 2);
-    __syncthreads();
-    if (kb + 1 >= kb1) break;
-    compute(1);
-    if (kb + 2 < kb1) store(0);
-    if (kb + 3 < kb1) load(kb + 3);
-    __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kGNST - 1; ++j)
+    if (kb0 + j < kb1) load(j, kb0 + j);
+  auto step = [&](int st, int kb) {
+    // stage kb's loads were issued before those of the next kGNST - 2 stages
+    wait_stages_after<NA + 2, 0, kGNST - 2>(min(kb1 - 1 - kb, kGNST - 2));
+    __syncthreads();  // stage kb visible to all waves; stage kb - 1 no longer read
+    if (kb + kGNST - 1 < kb1) load((st + kGNST - 1) % kGNST, kb + kGNST - 1);
+    compute(st);
+  };
+  for (int kb = kb0; kb < kb1; kb += kGNST) {
+#pragma unroll
+    for (int j = 0; j < kGNST; ++j)
+      if (kb + j < kb1) step(j, kb + j);
   }
 
-  // acc[mt][nt] register e: m = wm*128 + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*64 + nt*32 + l32
+  // acc[mt][nt] register e: m = wm*BM/2 + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*64 + nt*32 + l32
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const int m = mb * kGBM + wm * 128 + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+      const int m = mb * BM + wm * (BM / 2) + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
       if (m >= a.M) continue;
       if (SILU) {
         const int idx = nb * 128 + wn * 32 + l32;
@@ -721,6 +762,7 @@ struct GemmPlan {
   int kernel;
   int splits;
   int R = 0, D = 0;  // k_gemm_deep: weight fragments per block and register stages
+  int bm = 256;      // k_gemm_tiled: activation rows per block tile
 };
 
 template <int R, int MT, int D, bool SILU>
@@ -794,6 +836,34 @@ GemmPlan plan_deep(int M, int N, int K, bool silu, int max_splits) {
   return best;
 }
 
+// k_gemm_tiled plan: the block tile height (128 or 256 activation rows) and the
+// K split.  A block holds one CU (its LDS ring), so the time is set by rounds
+// of 256 blocks times the K steps of one block; per K step a BM = 128 block
+// takes 0.71 of a BM = 256 block (measured at 4k rows on the 7B shapes).  The
+// smaller tile pays where it saves padded rows or a round: 65-128 and
+// 257-384 rows of the gate/up projection, for instance.  Non-SiLU products
+// split K until the blocks fill one round, keeping >= 8 K steps per split.
+// The tile height does not depend on max_splits, so a launch with a capped
+// split recomputes the same one.
+GemmPlan plan_tiled(int M, int N, int K, bool silu, int max_splits) {
+  const int KB = K / kGBK;
+  GemmPlan best{kKTiled, 1};
+  double best_cost = 1e300;
+  for (int bm : {256, 128}) {
+    const int blocks = (silu ? N / 128 : (N + kGBN - 1) / kGBN) * ((M + bm - 1) / bm);
+    int s = silu ? 1 : std::max(1, 256 / blocks);
+    s = even_splits(KB, std::min(s, std::max(1, KB / 8)));
+    const int rounds = (blocks * s + 255) / 256;
+    const double cost = static_cast<double>(rounds) * ((KB + s - 1) / s) * (bm == 256 ? 1.0 : 0.71);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = GemmPlan{kKTiled, s, 0, 0, bm};
+    }
+  }
+  best.splits = even_splits(KB, std::min(best.splits, max_splits));
+  return best;
+}
+
 // Kernel and split choice, from sweeps of the Qwen2.5 decode shapes on
 // gfx950 (weights cycled through more than the 256 MB last-level cache so
 // that none is reused between launches): the deep-pipelined kernel for
@@ -802,13 +872,7 @@ GemmPlan plan_deep(int M, int N, int K, bool silu, int max_splits) {
 // projection at <= 16 rows), where launch latency dominates.
 GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
   if (!bf16) return {kKF32, 1};
-  if (M > 64) {
-    const int blocks = (silu ? N / 128 : (N + kGBN - 1) / kGBN) * ((M + kGBM - 1) / kGBM);
-    // one block per CU: the K split that keeps all blocks in one round of 256
-    int s = silu ? 1 : std::max(1, 256 / blocks);
-    s = std::min(s, std::max(1, (K / kGBK) / 4));
-    return {kKTiled, even_splits(K / kGBK, std::min(s, max_splits))};
-  }
+  if (M > 64) return plan_tiled(M, N, K, silu, max_splits);
   const double work = static_cast<double>(N) * K * (silu ? 2 : 1);
   if (K % 64 == 0 && N % 16 == 0 && work >= (M > 16 ? 8.0e6 : 1.4e7)) return plan_deep(M, N, K, silu, max_splits);
   const int n_chunks = K / 128;
@@ -851,19 +915,25 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
   }
   if (kernel == kKTiled || a.M > 64) {
     if (a.K % kGBK != 0 || (silu && a.N % 128 != 0) || (!silu && a.N % 8 != 0)) return hipErrorInvalidValue;
-    // 32-bit buffer offsets; every weight segment but the last a whole number of 8-row slabs
-    if (static_cast<int64_t>(a.M + kGBM) * a.lda * 2 >= (int64_t{1} << 31)) return hipErrorInvalidValue;
+    // 32-bit buffer offsets; every weight segment but the last a whole number of 16-row blocks
+    if (static_cast<int64_t>(a.M + 256) * a.lda * 2 >= (int64_t{1} << 31)) return hipErrorInvalidValue;
     for (int sg = 0; sg < a.W.n_seg; ++sg) {
       if (static_cast<int64_t>(a.W.rows[sg]) * a.K * 2 >= (int64_t{1} << 31)) return hipErrorInvalidValue;
-      if (!silu && sg < a.W.n_seg - 1 && a.W.rows[sg] % 8 != 0) return hipErrorInvalidValue;
+      if (!silu && sg < a.W.n_seg - 1 && a.W.rows[sg] % 16 != 0) return hipErrorInvalidValue;
     }
+    const int bm = a.M > 64 ? plan_tiled(a.M, a.N, a.K, silu, kMaxSplitsAny).bm : 256;
     const int kbps = (a.K / kGBK + a.splits - 1) / a.splits;
     const int n_nb = silu ? a.N / 128 : (a.N + kGBN - 1) / kGBN;
-    const int n_mb = (a.M + kGBM - 1) / kGBM;
+    const int n_mb = (a.M + bm - 1) / bm;
     const int per_xcd = (n_mb * n_nb + 7) / 8;
     dim3 grid(8 * per_xcd, a.splits);
-    if (silu) hipLaunchKernelGGL(k_gemm_tiled<true>, grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
-    else hipLaunchKernelGGL(k_gemm_tiled<false>, grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
+    if (bm == 128) {
+      if (silu) hipLaunchKernelGGL((k_gemm_tiled<128, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
+      else hipLaunchKernelGGL((k_gemm_tiled<128, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
+    } else {
+      if (silu) hipLaunchKernelGGL((k_gemm_tiled<256, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
+      else hipLaunchKernelGGL((k_gemm_tiled<256, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb);
+    }
     return hipGetLastError();
   }
   if (kernel == kKDeep) {

@@ -148,6 +148,31 @@ def test_bf16_decode_batch_shapes(model, layers, vocab, batches):
         assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, (B, r)
 
 
+def test_bf16_large_decode_batches():
+    """Decode batches above 64 rows run the LDS-tiled MFMA GEMM: 100 and 300 live rows take
+    128-row block tiles (the q/k/v, o and down products K-split), 200 rows 256-row tiles.  Every
+    row runs on the GPU; three per batch (first, middle, last: the ragged last block tile) are
+    compared with the oracle at the 7B layer shape."""
+    base = truncated(SHAPES["qwen2.5-7b"], 1, vocab=8192)
+    wd = make_weights(base, seed=2, device=DEV)
+    w64 = weights_to_numpy(wd)
+    rng = np.random.default_rng(6)
+    from workloads.gen import Workload
+    for B in (100, 200, 300):
+        plen = rng.integers(1, 24, size=B)
+        prompts = [rng.integers(0, base.vocab, size=int(p)).astype(np.int32) for p in plen]
+        offs = np.zeros(B + 1, np.int64)
+        offs[1:] = np.cumsum(plen)
+        wl = Workload("batch", base, np.arange(1000, 1000 + B, dtype=np.int64), np.concatenate(prompts), offs,
+                      np.full(B, 3, np.int32), np.arange(B, dtype=np.int32), 1.0, 78)
+        eng = _engine(base, wd, 320, 8192, 64, 2 * 320)
+        log(f"7b layer: decode batch B={B}")
+        r = teacher_forced_parity(eng, base, w64, wl, 3, 2e-2, 1.0, 78, check=[0, B // 2, B - 1])
+        eng.close()
+        log(f"B={B}: {r}")
+        assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, (B, r)
+
+
 def test_long_context_many_splits():
     """One 4150-token row beside two short ones: its decode context spans 65 pages, so the
     split-context attention runs 65 work items for that row and the merge walks two chunks
