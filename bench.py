@@ -30,6 +30,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode tokens/s/GPU + % peak HBM BW, Qwen2.5-7B-shape long-tail rollout"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFS = 2500.0  # dense bf16 MFMA, MI355X
+PREFILL_GEMMS = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down"]
 BF16_PEAK_TFLOPS = 2500.0
 WORKLOAD_TEXT = {
     "7b-long": "Qwen2.5-7B shape long round: 64 seqs, prompts U[128,1024], responses LogN(4096, 1.0) "
@@ -130,6 +132,30 @@ def measured_traffic(kernel: str, workload: str, path: str = TRAFFIC_RECORD):
     if rec.get("kernel") != kernel or rec.get("workload") != workload or rec.get("source_sha256") != digest:
         return None
     return int(rec["traffic_bytes_per_launch"])
+
+
+def prefill_mfma(eng, wl):
+    """MFMA utilisation of the prefill projections, from HIP events on the engine's stream: one untimed
+    prefill of every prompt of the workload (in chunks of max_prefill_tokens), the sequences then
+    aborted.  flops are 2*M*N*K per launch."""
+    import torch
+    eng.profile(PREFILL_GEMMS)
+    eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, np.maximum(wl.max_new, 2).astype(np.int32),
+                wl.sample_seed, wl.temperature)
+    torch.cuda.synchronize()
+    prof = [p for p in eng.profile_read() if p["phase"] == "prefill" and p["kernel"] in PREFILL_GEMMS]
+    eng.profile([])
+    eng.abort(wl.seq_ids)
+    eng.free_finished()
+    flops = sum(p["flops"] for p in prof)
+    ms = sum(p["total_ms"] for p in prof)
+    if ms <= 0:
+        return None
+    per = {p["kernel"]: round(p["flops"] / (p["total_ms"] * 1e-3) / 1e12, 1) for p in prof}
+    tfs = flops / (ms * 1e-3) / 1e12
+    return {"achieved": round(tfs, 1), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+            "frac": round(tfs / MFMA_BF16_PEAK_TFS, 4), "prompt_tokens": int(wl.prompt_lens().sum()),
+            "per_kernel_tflops": per}
 
 
 def main():
@@ -234,6 +260,8 @@ def main():
                    "rounds": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in s.items()} for s in last]},
         "roofline": roof,
     }
+    if shape.dtype == "bf16":
+        out["config"]["prefill_gemm_mfma"] = prefill_mfma(eng, wl)
     if args.compare_unscheduled and wl.round_id is not None:
         log("running the same sequences as one unscheduled batch")
         _, flat = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, wl.sample_seed,
