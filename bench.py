@@ -17,7 +17,6 @@ a single GPU.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -121,15 +120,16 @@ TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gate_up_traffic.json")
 def measured_traffic(kernel: str, workload: str, path: str = TRAFFIC_RECORD):
     """HBM bytes per launch of the roofline kernel from the calibrated FETCH_SIZE / WRITE_SIZE
     counter runs recorded in profiles/, or None when there is no record for this kernel and
-    workload or the kernel's source has changed since the counters were taken."""
+    workload or the kernel (its source text and launch plan) has changed since the counters were
+    taken."""
+    from paper_2509_21009_amd.counter_traffic import deep_source_digest
     try:
         with open(path) as f:
             rec = json.load(f)
-        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
-            digest = hashlib.sha256(f.read()).hexdigest()
+        digest = deep_source_digest(ROOT)
     except (OSError, ValueError, KeyError):
         return None
-    if rec.get("kernel") != kernel or rec.get("workload") != workload or rec.get("source_sha256") != digest:
+    if rec.get("kernel") != kernel or rec.get("workload") != workload or rec.get("source_sha256_deep") != digest:
         return None
     return int(rec["traffic_bytes_per_launch"])
 

@@ -6,8 +6,8 @@ and four 16-row activation tiles), and the ``--kernel-trace --stats``
 kernel_stats CSV of the benchmark round whose launch mix weights them.  Each
 profile_steps run ends with a 1 GiB device copy; its counter readings
 calibrate FETCH_SIZE and WRITE_SIZE (KiB per dispatch) to bytes.  Writes the
-record bench.py reads (kernel, workload, SHA-256 of the kernel source, bytes
-per launch) and prints a table for the profile summary.  From the repository
+record bench.py reads (kernel, workload, SHA-256 of the deep kernel's source
+text and launch plan, bytes per launch) and prints a table for the profile summary.  From the repository
 root:
 
     python3 paper_2509_21009_amd/counter_traffic.py --pmc-dir gpurun_out \\
@@ -25,6 +25,25 @@ import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SOURCE = "paper_2509_21009_amd/csrc/k_gemm.hip"
+COMMON = "paper_2509_21009_amd/csrc/device_common.hpp"
+
+
+def _between(text: str, start: str, end: str) -> str:
+    i = text.index(start)
+    return text[i:text.index(end, i) + len(end)]
+
+
+def deep_source_digest(root: str = ROOT) -> str:
+    """SHA-256 over what the counters measured: the k_gemm_deep kernel, its launch plan (the
+    instantiated configurations and plan_deep) and the device helpers it uses.  Edits elsewhere in
+    the GEMM source leave it unchanged."""
+    gemm = open(os.path.join(root, SOURCE)).read()
+    parts = [_between(gemm, "template <int R, int MT, int D, bool SILU>\n__global__ __launch_bounds__(256) "
+                            "void k_gemm_deep", "\n}\n"),
+             _between(gemm, "constexpr DeepCfg kDeepCfg", "\n};\n"),
+             _between(gemm, "GemmPlan plan_deep(", "\n}\n"),
+             open(os.path.join(root, COMMON)).read()]
+    return hashlib.sha256("\n".join(parts).encode()).hexdigest()
 COPY_BYTES = 1 << 30
 SHAPE = {"H": 3584, "I": 18944}  # Qwen2.5-7B hidden and intermediate sizes
 
@@ -75,8 +94,8 @@ def main():
     traffic = sum(per_tile[t] * c for t, c in mix.items()) / total
     alg_mix = sum((2 * SHAPE["I"] * SHAPE["H"] * 2 + 16 * t * (SHAPE["H"] + SHAPE["I"]) * 2) * c
                   for t, c in mix.items()) / total
-    digest = hashlib.sha256(open(os.path.join(ROOT, SOURCE), "rb").read()).hexdigest()
-    rec = {"kernel": "gemm_gate_up", "workload": "7b-long", "source": SOURCE, "source_sha256": digest,
+    rec = {"kernel": "gemm_gate_up", "workload": "7b-long", "source": SOURCE,
+           "source_sha256_deep": deep_source_digest(),
            "traffic_bytes_per_launch": int(round(traffic)),
            "per_tile_count": {str(t): int(round(v)) for t, v in sorted(per_tile.items())},
            "launch_mix": {str(t): c for t, c in sorted(mix.items())},

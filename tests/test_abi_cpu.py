@@ -184,22 +184,32 @@ def test_tail_batched_rollout_rejects_null_engine(lib):
 
 def test_bench_reports_counter_traffic_only_for_the_measured_kernel(tmp_path):
     """roofline.traffic comes from a calibrated counter record and is dropped when the workload
-    or kernel differs or the kernel source no longer matches the recorded hash."""
-    import hashlib
+    or kernel differs or the deep kernel's source no longer matches the recorded hash."""
     import json
     import bench
-    src = "paper_2509_21009_amd/csrc/k_gemm.hip"
-    digest = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
-    rec = {"kernel": "gemm_gate_up", "workload": "7b-long", "source": src, "source_sha256": digest,
-           "traffic_bytes_per_launch": 123456}
+    from paper_2509_21009_amd.counter_traffic import COMMON, SOURCE, deep_source_digest
+    rec = {"kernel": "gemm_gate_up", "workload": "7b-long", "source": SOURCE,
+           "source_sha256_deep": deep_source_digest(ROOT), "traffic_bytes_per_launch": 123456}
     path = tmp_path / "rec.json"
     path.write_text(json.dumps(rec))
     assert bench.measured_traffic("gemm_gate_up", "7b-long", str(path)) == 123456
     assert bench.measured_traffic("gemm_gate_up", "7b-short", str(path)) is None
     assert bench.measured_traffic("gemm_down", "7b-long", str(path)) is None
-    path.write_text(json.dumps(dict(rec, source_sha256="0" * 64)))
+    path.write_text(json.dumps(dict(rec, source_sha256_deep="0" * 64)))
     assert bench.measured_traffic("gemm_gate_up", "7b-long", str(path)) is None
     assert bench.measured_traffic("gemm_gate_up", "7b-long", str(tmp_path / "missing.json")) is None
+    # the digest covers the deep kernel and its plan, not the rest of the GEMM source
+    root = tmp_path / "tree"
+    for rel in (SOURCE, COMMON):
+        (root / rel).parent.mkdir(parents=True, exist_ok=True)
+        (root / rel).write_text(open(os.path.join(ROOT, rel)).read())
+    base = deep_source_digest(str(root))
+    assert base == deep_source_digest(ROOT)
+    gemm = (root / SOURCE).read_text()
+    (root / SOURCE).write_text(gemm.replace("constexpr int kGBN = 256", "constexpr int kGBN = 256  /* edit */"))
+    assert deep_source_digest(str(root)) == base
+    (root / SOURCE).write_text(gemm.replace("const int K = a.K, KU = K / 64;", "const int K = a.K, KU = K / 64;  // edit"))
+    assert deep_source_digest(str(root)) != base
     # the committed record names the kernel bench.py reports by default
     committed = json.load(open(bench.TRAFFIC_RECORD))
     assert committed["kernel"] == "gemm_gate_up" and committed["workload"] == "7b-long"
