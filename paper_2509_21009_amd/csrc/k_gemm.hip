@@ -22,7 +22,7 @@
 //    the consumer kernel sums.
 //  * k_gemm_tiled (M > 64: prefill and large decode batches): 128- or
 //    256-row x 256 block tiles, 2x4 waves of 32x32x16 MFMAs, tiles loaded
-//    from global memory straight into a 4-stage swizzled LDS ring.
+//    from global memory straight into a 3-stage swizzled LDS ring.
 //  * k_gemm_f32: fp32 FMA tiles for the fp32 model (no reduced precision).
 //
 // The SiLU epilogue pairs gate row i with up row i in one thread and writes
@@ -473,7 +473,7 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
 // 8 for wide products (>= 64 panels: gate/up, the LM head) and 2 for
 // narrow ones (measured: at 4k-16k rows gate/up gains 4 points of MFMA peak
 // over a single panel at a time, q/k/v, o and down 2-4).
-constexpr int kGBN = 256, kGBK = 32, kGNST = 4;
+constexpr int kGBN = 256, kGBK = 32, kGNST = 3;
 
 typedef uint32_t u32x4_raw __attribute__((ext_vector_type(4)));
 // Buffer descriptor with the same fields as buffer_rsrc (base, stride 0, size, flags), as the
