@@ -21,8 +21,8 @@
 //    through LDS; blockIdx.y splits K further and writes fp32 partials that
 //    the consumer kernel sums.
 //  * k_gemm_tiled (M > 64: prefill and large decode batches): 128- or
-//    256-row x 256 block tiles, 2x4 waves of 32x32x16 MFMAs, tiles loaded
-//    from global memory straight into a 3-stage swizzled LDS ring.
+//    256-row x 128- or 256-row block tiles, 8 waves of 32x32x16 MFMAs, tiles
+//    loaded from global memory straight into a 3-stage swizzled LDS ring.
 //  * k_gemm_f32: fp32 FMA tiles for the fp32 model (no reduced precision).
 //
 // The SiLU epilogue pairs gate row i with up row i in one thread and writes
@@ -448,8 +448,9 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
 }
 
 // ---- prefill / large-batch tiled MFMA GEMM ---------------------------------
-// Block tile: BM activation rows (m, 128 or 256) x 256 weight rows (n), K step
-// 32, eight waves as 2 (m) x 4 (n), each computing BM/2 m x 64 n with
+// Block tile: BM activation rows (m, 128 or 256) x BN weight rows (n, 128 or
+// 256), K step 32, eight waves as 2 (m) x 4 (n) for BN = 256 or 4 x 2 for
+// BN = 128, each computing BM/2 or BM/4 m x 64 n with
 // v_mfma_f32_32x32x16_bf16 (two waves per SIMD).  Activations are the MFMA
 // row operand and weights the column operand, so the 32 lanes of one
 // accumulator register hold 32 consecutive n: coalesced stores.
@@ -473,7 +474,7 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
 // 8 for wide products (>= 64 panels: gate/up, the LM head) and 2 for
 // narrow ones (measured: at 4k-16k rows gate/up gains 4 points of MFMA peak
 // over a single panel at a time, q/k/v, o and down 2-4).
-constexpr int kGBN = 256, kGBK = 32, kGNST = 3;
+constexpr int kGBK = 32, kGNST = 3;
 
 typedef uint32_t u32x4_raw __attribute__((ext_vector_type(4)));
 // Buffer descriptor with the same fields as buffer_rsrc (base, stride 0, size, flags), as the
@@ -504,11 +505,14 @@ __device__ __forceinline__ void wait_stages_after(int after) {
 }
 __device__ __forceinline__ int gswz(int r) { return (r >> 2) & 3; }
 
-template <int BM, bool SILU>
+template <int BM, int BN, bool SILU>
 __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_split, int n_mb, int n_nb, int gm) {
-  constexpr int STAGE = (BM + kGBN) * kGBK;  // elements per stage
-  constexpr int MT = BM / 64;                // 32-row activation tiles per wave
-  constexpr int NA = BM / 128;               // 16-row activation blocks a wave loads per stage
+  constexpr int STAGE = (BM + BN) * kGBK;       // elements per stage
+  constexpr int WMW = BN == 256 ? 2 : 4;        // waves along m (8 waves: WMW x 8 / WMW)
+  constexpr int WROWS = BM / WMW;               // activation rows per wave
+  constexpr int MT = WROWS / 32;                // 32-row activation tiles per wave
+  constexpr int NA = BM / 128, NW = BN / 128;   // 16-row blocks of activations / weights a wave loads per stage
+  static_assert(MT >= 1 && (BN == 128 || BN == 256), "tile shape");
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kGNST * STAGE];
   const int n_tiles = n_mb * n_nb;
   const int per_xcd = (n_tiles + 7) / 8;
@@ -520,33 +524,33 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
   const int split = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % WMW, wn = wave / WMW;
   const int l32 = lane & 31, lh = lane >> 5;
   const int K = a.K;
 
   // Loads: wave w fills 16-row blocks w + 8 i of each tile; lane -> row lane >> 2 of the block,
   // LDS chunk lane & 3, which holds global chunk (lane & 3) ^ gswz(row).
   const u32x4_raw ars = raw_rsrc(a.A, static_cast<uint32_t>(a.M) * static_cast<uint32_t>(a.lda) * 2u);
-  int aoff[NA], woff[2];
-  u32x4_raw wrs[2];
+  int aoff[NA], woff[NW];
+  u32x4_raw wrs[NW];
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
     const int r = (wave + 8 * i) * 16 + (lane >> 2);
     aoff[i] = ((mb * BM + r) * static_cast<int>(a.lda) + ((lane & 3) ^ gswz(r)) * 8) * 2;
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < NW; ++i) {
     const int r0 = (wave + 8 * i) * 16;
     const int r = r0 + (lane >> 2);
     const bf16_t* wb;
     int rel0, rows_valid;
     if (SILU) {  // 32-row groups alternate gate / up over the same output indices
-      const int grp = r0 >> 5;
-      wb = static_cast<const bf16_t*>(a.W.ptr[grp & 1]);
-      rel0 = nb * 128 + (grp >> 1) * 32 + (r0 & 31);
+      const int g32 = r0 >> 5;
+      wb = static_cast<const bf16_t*>(a.W.ptr[g32 & 1]);
+      rel0 = nb * (BN / 2) + (g32 >> 1) * 32 + (r0 & 31);
       rows_valid = a.N;
     } else {
-      const int n0 = nb * kGBN + r0;
+      const int n0 = nb * BN + r0;
       int b = 0, sg = 0;
       while (sg < a.W.n_seg - 1 && n0 >= b + a.W.rows[sg]) b += a.W.rows[sg++];
       wb = static_cast<const bf16_t*>(a.W.ptr[sg]);
@@ -576,7 +580,7 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
     for (int i = 0; i < NA; ++i)
       dma16(ars, __builtin_amdgcn_readfirstlane(sa + static_cast<uint32_t>((wave + 8 * i) * 1024)), aoff[i] + ko);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NW; ++i)
       dma16(wrs[i], __builtin_amdgcn_readfirstlane(sw + static_cast<uint32_t>((wave + 8 * i) * 1024)), woff[i] + ko);
   };
   auto compute = [&](int st) {
@@ -587,7 +591,7 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
       const int c = ki * 2 + lh;  // the lane's 16-byte chunk of this k-step
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int r = wm * (BM / 2) + mt * 32 + l32;
+        const int r = wm * WROWS + mt * 32 + l32;
         af[buf][mt] = *reinterpret_cast<const bf16x8_t*>(sA + r * kGBK + (c ^ gswz(r)) * 8);
       }
 #pragma unroll
@@ -608,12 +612,14 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma32x32x16(af[ki & 1][mt], bw[ki & 1][nt], acc[mt][nt]);
       if (ki + 1 < kGBK / 16) {
+        constexpr int NRD = MT + 2, NMF = 2 * MT, NP = NRD < NMF ? NRD : NMF;
 #pragma unroll
-        for (int q = 0; q < MT + 2; ++q) {
+        for (int q = 0; q < NP; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
         }
-        if constexpr (MT > 2) __builtin_amdgcn_sched_group_barrier(0x008, MT - 2, 0);
+        if constexpr (NMF > NP) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NP, 0);
+        if constexpr (NRD > NP) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NP, 0);
       }
       __builtin_amdgcn_s_setprio(0);
     }
@@ -623,7 +629,7 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
     if (kb0 + j < kb1) load(j, kb0 + j);
   auto step = [&](int st, int kb) {
     // stage kb's loads were issued before those of the next kGNST - 2 stages
-    wait_stages_after<NA + 2, 0, kGNST - 2>(min(kb1 - 1 - kb, kGNST - 2));
+    wait_stages_after<NA + NW, 0, kGNST - 2>(min(kb1 - 1 - kb, kGNST - 2));
     __syncthreads();  // stage kb visible to all waves; stage kb - 1 no longer read
     if (kb + kGNST - 1 < kb1) load((st + kGNST - 1) % kGNST, kb + kGNST - 1);
     compute(st);
@@ -634,22 +640,22 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
       if (kb + j < kb1) step(j, kb + j);
   }
 
-  // acc[mt][nt] register e: m = wm*BM/2 + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*64 + nt*32 + l32
+  // acc[mt][nt] register e: m = wm*WROWS + mt*32 + 8*(e/4) + 4*lh + e%4, n = wn*64 + nt*32 + l32
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const int m = mb * BM + wm * (BM / 2) + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+      const int m = mb * BM + wm * WROWS + mt * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
       if (m >= a.M) continue;
       if (SILU) {
-        const int idx = nb * 128 + wn * 32 + l32;
+        const int idx = nb * (BN / 2) + wn * 32 + l32;
         static_cast<bf16_t*>(a.act_out)[static_cast<size_t>(m) * a.N + idx] =
             f32_to_bf16(silu(acc[mt][0][e]) * acc[mt][1][e]);
       } else {
         float* out = a.part + (static_cast<size_t>(split) * a.M + m) * a.N;
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
-          const int n = nb * kGBN + wn * 64 + nt * 32 + l32;
+          const int n = nb * BN + wn * 64 + nt * 32 + l32;
           if (n < a.N) out[n] = acc[mt][nt][e];
         }
       }
@@ -769,6 +775,7 @@ struct GemmPlan {
   int splits;
   int R = 0, D = 0;  // k_gemm_deep: weight fragments per block and register stages
   int bm = 256;      // k_gemm_tiled: activation rows per block tile
+  int bn = 256;      // k_gemm_tiled: weight rows per block tile
 };
 
 template <int R, int MT, int D, bool SILU>
@@ -842,28 +849,34 @@ GemmPlan plan_deep(int M, int N, int K, bool silu, int max_splits) {
   return best;
 }
 
-// k_gemm_tiled plan: the block tile height (128 or 256 activation rows) and the
-// K split.  A block holds one CU (its LDS ring), so the time is set by rounds
-// of 256 blocks times the K steps of one block; per K step a BM = 128 block
-// takes 0.71 of a BM = 256 block (measured at 4k rows on the 7B shapes).  The
-// smaller tile pays where it saves padded rows or a round: 65-128 and
-// 257-384 rows of the gate/up projection, for instance.  Non-SiLU products
-// split K until the blocks fill one round, keeping >= 8 K steps per split.
-// The tile height does not depend on max_splits, so a launch with a capped
-// split recomputes the same one.
+// k_gemm_tiled plan: the block tile (BM activation rows x BN weight rows) and
+// the K split.  A block holds one CU's LDS ring and the 8 waves of two
+// SIMD-pairs, so the time is set by rounds of 256 blocks times the K steps of
+// one block; per K step a BM = 128 block takes 0.71 of a BM = 256 block
+// (measured at 4k rows on the 7B shapes).  The smaller tile pays where it
+// saves padded rows or a round: 65-128 and 257-384 rows of the gate/up
+// projection, for instance.  Non-SiLU products split K until the blocks fill
+// one round, keeping >= 8 K steps per split.  At decode batches (<= 512 rows)
+// they take 128-row weight panels: twice the panels for the same blocks, so
+// half the split and half its fp32 partial traffic, which at these sizes
+// exceeds the weights themselves (q/k/v at 256 rows and 14 splits: 66 MB of
+// partials for 33 MB of weights); measured 1.15-1.9x faster there.  The tile
+// does not depend on max_splits, so a launch with a capped split recomputes
+// the same one.
 GemmPlan plan_tiled(int M, int N, int K, bool silu, int max_splits) {
   const int KB = K / kGBK;
+  const int bn = (!silu && M <= 512) ? 128 : 256;
   GemmPlan best{kKTiled, 1};
   double best_cost = 1e300;
   for (int bm : {256, 128}) {
-    const int blocks = (silu ? N / 128 : (N + kGBN - 1) / kGBN) * ((M + bm - 1) / bm);
+    const int blocks = (silu ? N / (bn / 2) : (N + bn - 1) / bn) * ((M + bm - 1) / bm);
     int s = silu ? 1 : std::max(1, 256 / blocks);
     s = even_splits(KB, std::min(s, std::max(1, KB / 8)));
     const int rounds = (blocks * s + 255) / 256;
     const double cost = static_cast<double>(rounds) * ((KB + s - 1) / s) * (bm == 256 ? 1.0 : 0.71);
     if (cost < best_cost) {
       best_cost = cost;
-      best = GemmPlan{kKTiled, s, 0, 0, bm};
+      best = GemmPlan{kKTiled, s, 0, 0, bm, bn};
     }
   }
   best.splits = even_splits(KB, std::min(best.splits, max_splits));
@@ -927,20 +940,22 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
       if (static_cast<int64_t>(a.W.rows[sg]) * a.K * 2 >= (int64_t{1} << 31)) return hipErrorInvalidValue;
       if (!silu && sg < a.W.n_seg - 1 && a.W.rows[sg] % 16 != 0) return hipErrorInvalidValue;
     }
-    const int bm = a.M > 64 ? plan_tiled(a.M, a.N, a.K, silu, kMaxSplitsAny).bm : 256;
+    GemmPlan tp{kKTiled, 1};
+    if (a.M > 64) tp = plan_tiled(a.M, a.N, a.K, silu, kMaxSplitsAny);
+    const int bm = tp.bm, bn = tp.bn;
     const int kbps = (a.K / kGBK + a.splits - 1) / a.splits;
-    const int n_nb = silu ? a.N / 128 : (a.N + kGBN - 1) / kGBN;
+    const int n_nb = silu ? a.N / (bn / 2) : (a.N + bn - 1) / bn;
     const int n_mb = (a.M + bm - 1) / bm;
     const int per_xcd = (n_mb * n_nb + 7) / 8;
     const int gm = n_nb >= 64 ? 8 : 2;
     dim3 grid(8 * per_xcd, a.splits);
-    if (bm == 128) {
-      if (silu) hipLaunchKernelGGL((k_gemm_tiled<128, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm);
-      else hipLaunchKernelGGL((k_gemm_tiled<128, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm);
-    } else {
-      if (silu) hipLaunchKernelGGL((k_gemm_tiled<256, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm);
-      else hipLaunchKernelGGL((k_gemm_tiled<256, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm);
+#define RP_TILED(BM_, BN_)                                                                                   \
+    if (bm == BM_ && bn == BN_) {                                                                            \
+      if (silu) hipLaunchKernelGGL((k_gemm_tiled<BM_, BN_, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
+      else hipLaunchKernelGGL((k_gemm_tiled<BM_, BN_, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
     }
+    RP_TILED(128, 128) RP_TILED(128, 256) RP_TILED(256, 128) RP_TILED(256, 256)
+#undef RP_TILED
     return hipGetLastError();
   }
   if (kernel == kKDeep) {
