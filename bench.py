@@ -134,6 +134,19 @@ def measured_traffic(kernel: str, workload: str, path: str = TRAFFIC_RECORD):
     return int(rec["traffic_bytes_per_launch"])
 
 
+def measured_stream_gbs(gib: float = 2.0, reps: int = 5) -> float:
+    """The practical HBM read ceiling on this device (rp_stream_read_gbs: the library's streaming
+    read kernel over a `gib` GiB buffer, far past the 256 MB last-level cache, fastest of `reps`)."""
+    import torch
+    from paper_2509_21009_amd import rollpack as rp
+    x = torch.empty(int(gib * (1 << 30)), dtype=torch.uint8, device="cuda")
+    x.fill_(1)
+    gbs = rp.rp_stream_read_gbs(x, reps)
+    del x
+    torch.cuda.empty_cache()
+    return gbs
+
+
 def prefill_mfma(eng, wl):
     """MFMA utilisation of the prefill projections, from HIP events on the engine's stream: one untimed
     prefill of every prompt of the workload (in chunks of max_prefill_tokens), the sequences then
@@ -260,6 +273,13 @@ def main():
                    "rounds": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in s.items()} for s in last]},
         "roofline": roof,
     }
+    if len(all_stats) > 1:
+        out["config"]["round_makespan_median_s"] = round(float(np.median(
+            [sum(s_["makespan_ms"] for s_ in st) / 1e3 for st in all_stats])), 3)
+    if roof is not None:
+        stream = measured_stream_gbs()
+        roof["measured_peak"] = round(stream, 1)
+        roof["frac_measured"] = round(roof["achieved"] / stream, 4)
     if shape.dtype == "bf16":
         out["config"]["prefill_gemm_mfma"] = prefill_mfma(eng, wl)
     if args.compare_unscheduled and wl.round_id is not None:

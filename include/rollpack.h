@@ -380,6 +380,18 @@ rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask);
  * record per (class, phase) with launches > 0, into host out [cap]. */
 rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int32_t* n_out);
 
+/* The practical HBM read ceiling that measurement reports next to the nominal
+ * peak (the roofline of the memory-bound decode kernels): streams the
+ * caller's device buffer dev_buf (bytes >= 1 MiB, 16-byte aligned; its
+ * contents are read, never written) reps times with a read-only kernel in
+ * which each of 2048 waves walks its own contiguous share with 8 one-KB loads
+ * in flight, on hip_stream, and returns
+ * the fastest pass in GB/s (1e9 bytes/s) through gbs_out.  Blocks the calling
+ * thread; needs no engine and allocates no device memory.  A buffer larger
+ * than the 256 MB last-level cache measures HBM.  Errors: RP_ERR_INVALID_ARG
+ * on bad arguments, RP_ERR_HIP if a launch or event call fails. */
+rp_status rp_stream_read_gbs(const void* dev_buf, size_t bytes, int32_t reps, void* hip_stream, double* gbs_out);
+
 /* One step of the engine: a decode step over `rows` sequences with
  * `sum_ctx` context tokens in total, or one prefill chunk of `rows` tokens
  * (sum_ctx then counts the keys its queries attend to).  ms is the HIP-event

@@ -448,6 +448,37 @@ hipError_t launch_sample(const SampleArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Streaming read of a buffer: each wave walks its own contiguous share, 8 one-KB loads (16 bytes
+// per lane) in flight per step, 8 waves per CU: the practical HBM read ceiling that measurement
+// reports next to the nominal peak.  The values feed an empty asm so that every load is issued.
+constexpr int kStreamWaves = 2048;
+
+__global__ __launch_bounds__(256) void k_stream_read(const uint4* p, size_t n16) {
+  const int lane = threadIdx.x & 63;
+  const size_t wave = static_cast<size_t>(blockIdx.x) * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const size_t share = (n16 / 64 / kStreamWaves) * 64;  // whole 1 KB runs per wave
+  const size_t begin = wave * share, end = begin + share;
+  uint32_t acc = 0;
+  size_t i = begin + lane;
+  for (; i + 7 * 64 < end; i += 8 * 64) {
+    uint4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = p[i + j * 64];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+  }
+  for (; i < end; i += 64) acc ^= p[i].x;
+  for (size_t t = kStreamWaves * share + wave * 64 + lane; t < n16; t += static_cast<size_t>(kStreamWaves) * 64)
+    acc ^= p[t].x;  // the remainder past the waves' equal shares
+  asm volatile("" : : "v"(acc));
+}
+
+hipError_t launch_stream_read(const void* buf, size_t bytes, hipStream_t s) {
+  if (bytes < 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_stream_read, dim3(kStreamWaves / 4), dim3(256), 0, s, static_cast<const uint4*>(buf), bytes / 16);
+  return hipGetLastError();
+}
+
 hipError_t launch_gather_rows(const void* src, const int32_t* rows, int n, int H, int esize, void* out,
                               hipStream_t s) {
   if (n <= 0) return hipSuccess;

@@ -130,6 +130,8 @@ hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
 int sample_chunks(int V);
 
 // out[i, :] = src[rows[i], :] for i < n (element size esize bytes, H elements)
+// Reads bytes / 16 x 16 bytes of buf (16-byte aligned) once, with nothing written.
+hipError_t launch_stream_read(const void* buf, size_t bytes, hipStream_t s);
 hipError_t launch_gather_rows(const void* src, const int32_t* rows, int n, int H, int esize,
                               void* out, hipStream_t s);
 

@@ -245,6 +245,35 @@ rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int
   });
 }
 
+rp_status rp_stream_read_gbs(const void* dev_buf, size_t bytes, int32_t reps, void* hip_stream, double* gbs_out) {
+  return guarded([&] {
+    if (!dev_buf || bytes < (size_t{1} << 20) || reinterpret_cast<uintptr_t>(dev_buf) % 16 || reps < 1 || !gbs_out)
+      throw rollpack::RpError(RP_ERR_INVALID_ARG, "stream read: need a 16-byte aligned buffer of >= 1 MiB, reps >= 1");
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    auto check = [](hipError_t e, const char* what) {
+      if (e != hipSuccess) throw rollpack::RpError(RP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+    };
+    hipEvent_t e0, e1;
+    check(hipEventCreate(&e0), "hipEventCreate");
+    check(hipEventCreate(&e1), "hipEventCreate");
+    float best = 0.f;
+    hipError_t err = rollpack::launch_stream_read(dev_buf, bytes, s);  // warm-up
+    for (int32_t r = 0; r < reps && err == hipSuccess; ++r) {
+      err = hipEventRecord(e0, s);
+      if (err == hipSuccess) err = rollpack::launch_stream_read(dev_buf, bytes, s);
+      if (err == hipSuccess) err = hipEventRecord(e1, s);
+      if (err == hipSuccess) err = hipEventSynchronize(e1);
+      float ms = 0.f;
+      if (err == hipSuccess) err = hipEventElapsedTime(&ms, e0, e1);
+      if (err == hipSuccess && (best == 0.f || ms < best)) best = ms;
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    check(err, "stream read");
+    *gbs_out = static_cast<double>(bytes / 16 * 16) / (best * 1e-3) / 1e9;
+  });
+}
+
 const char* rp_last_error(void) { return g_last_error.c_str(); }
 
 }  // extern "C"

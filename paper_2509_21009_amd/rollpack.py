@@ -119,6 +119,7 @@ SIGNATURES = {
     "rp_step_trace_read": (ctypes.c_int, [_P, ctypes.POINTER(RpStepRecord), ctypes.c_int32, _I32P]),
     "rp_profile_enable": (ctypes.c_int, [_P, ctypes.c_uint32]),
     "rp_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(RpKernelStats), ctypes.c_int32, _I32P]),
+    "rp_stream_read_gbs": (ctypes.c_int, [_P, ctypes.c_size_t, ctypes.c_int32, _P, ctypes.POINTER(ctypes.c_double)]),
     "rp_last_error": (ctypes.c_char_p, []),
 }
 
@@ -364,6 +365,17 @@ def rp_profile_read(eng: int, cap: int = 64):
     n = ctypes.c_int32()
     _check(load_library().rp_profile_read(eng, out, cap, ctypes.byref(n)))
     return [out[i].as_dict() for i in range(n.value)]
+
+
+def rp_stream_read_gbs(buf, reps: int = 5) -> float:
+    """HBM read ceiling in GB/s: the fastest of `reps` streaming reads of the device tensor `buf`
+    (contiguous; use more than 256 MB so that the last-level cache does not hold it)."""
+    import torch
+    gbs = ctypes.c_double()
+    stream = torch.cuda.current_stream(buf.device).cuda_stream
+    _check(load_library().rp_stream_read_gbs(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                                             reps, ctypes.c_void_p(stream), ctypes.byref(gbs)))
+    return gbs.value
 
 
 def rp_last_error() -> str:

@@ -264,3 +264,18 @@ def test_engine_errors_leave_state_unchanged(tiny):
     eng.prefill(np.array([2, 3], np.int64), np.concatenate([p, p]), np.array([0, 10, 20], np.int64),
                 np.array([50, 50], np.int32))                 # the pages came back
     eng.close()
+
+
+def test_stream_read_ceiling():
+    """rp_stream_read_gbs: a read-only streaming pass over a 1 GiB buffer reports a plausible HBM
+    rate, leaves the buffer unchanged, and rejects buffers under 1 MiB."""
+    R = rp()
+    x = torch.arange(1 << 28, dtype=torch.int32, device=DEV)
+    before = int(x[::4096].sum().item())
+    gbs = R.rp_stream_read_gbs(x, 3)
+    log(f"stream read: {gbs:.0f} GB/s")
+    assert 1000.0 < gbs < 8000.0
+    assert int(x[::4096].sum().item()) == before
+    with pytest.raises(R.RollpackError):
+        R.rp_stream_read_gbs(torch.zeros(1024, dtype=torch.int32, device=DEV), 1)
+
