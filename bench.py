@@ -179,6 +179,8 @@ def main():
     ap.add_argument("--workload", default="7b-long", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--kernel", default="gemm_gate_up", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-every", type=int, default=8,
+                    help="time one launch in N of the roofline kernel inside the timed rounds (1: all)")
     ap.add_argument("--max-prefill-tokens", type=int, default=16384)
     ap.add_argument("--step-trace", default=None, metavar="PATH",
                     help="after the timed steps, run one more (untimed) round with the per-step trace on and write "
@@ -223,7 +225,7 @@ def main():
         t0 = time.perf_counter()
         call()
         log(f"warmup step {i + 1}/{args.warmup} done in {time.perf_counter() - t0:.1f} s")
-    eng.profile([args.kernel])
+    eng.profile([args.kernel], every=args.profile_every)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     all_stats = []
@@ -258,7 +260,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.kernel, args.workload),
                 "kernel": args.kernel,
-                "phase": "decode", "launches": p["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
+                "phase": "decode", "launches": p["launches"], "timed_every": args.profile_every,
+                "avg_launch_us": round(avg_ms * 1e3, 2),
                 "algorithmic_bytes_per_launch": bytes_per}
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,

@@ -371,10 +371,20 @@ typedef struct rp_kernel_stats {
 
 /* Per-kernel timing, the measurement side of the paper's offline profiling
  * phase (section 4.1: prefill and decode throughput against batch size and
- * sequence length).  class_mask selects the classes whose launches are
- * bracketed by HIP events from now on (0 stops).  Bracketing adds a little
- * host work per selected launch; unselected launches are untouched. */
+ * sequence length).  class_mask selects the classes whose launches are timed
+ * from now on (0 stops): the launch's own dispatch stamps a pair of HIP
+ * events with its first kernel's start and its last kernel's end.  Timing
+ * adds a little host work per selected launch, and the stamped dispatches
+ * cost the GPU a few microseconds each; unselected launches are untouched.
+ * Every class starts timing all of its launches (see rp_profile_every). */
 rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask);
+
+/* Time only one launch in `every` (>= 1) of each selected class: the first,
+ * then every `every`-th, counted per class and phase from this call.  The
+ * statistics then cover the timed launches only (launches, total_ms, bytes
+ * and flops alike), so averages stay unbiased when the sampled launches
+ * spread over the workload.  RP_ERR_INVALID_ARG for every < 1. */
+rp_status rp_profile_every(rp_engine* eng, int32_t every);
 
 /* Synchronise, then report and reset the accumulated measurements: one
  * record per (class, phase) with launches > 0, into host out [cap]. */

@@ -381,7 +381,7 @@ Waiting* Engine::find_waiting(int64_t id) {
 
 template <typename F>
 void Engine::launch_timed(int cls, double bytes, double flops, F&& launch) {
-  if (!(prof_mask_ & (1u << cls))) {
+  if (!(prof_mask_ & (1u << cls)) || prof_seen_[cls][phase_]++ % prof_every_ != 0) {
     HIP_TRY(launch());
     return;
   }
@@ -395,10 +395,20 @@ void Engine::launch_timed(int cls, double bytes, double flops, F&& launch) {
     prof_pool_.pop_back();
     return e;
   };
+  // The kernels stamp the events from their own dispatch: no marker packets
+  // between kernels, so profiling does not slow the step it measures.
   hipEvent_t e0 = take(), e1 = take();
-  HIP_TRY(hipEventRecord(e0, stream_));
-  HIP_TRY(launch());
-  HIP_TRY(hipEventRecord(e1, stream_));
+  LaunchEvents& ev = launch_events();
+  ev = LaunchEvents{e0, e1};
+  const hipError_t err = launch();
+  const bool launched = ev.start == nullptr;
+  ev = LaunchEvents{};
+  HIP_TRY(err);
+  if (!launched) {  // nothing to do (an empty batch): no kernel, no stamps
+    prof_pool_.push_back(e0);
+    prof_pool_.push_back(e1);
+    return;
+  }
   prof_pending_.push_back({cls, phase_, e0, e1, bytes, flops});
   if (prof_pending_.size() >= 4096) prof_harvest();
 }
@@ -807,6 +817,12 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     if (q.n_gen >= q.max_new) q.finished = true;
   }
   return B;
+}
+
+void Engine::profile_every(int32_t every) {
+  if (every < 1) throw RpError(RP_ERR_INVALID_ARG, "profile sampling: every must be >= 1");
+  prof_every_ = every;
+  for (auto& c : prof_seen_) c[0] = c[1] = 0;
 }
 
 void Engine::profile_enable(uint32_t mask) {

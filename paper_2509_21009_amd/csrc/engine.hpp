@@ -134,6 +134,7 @@ class Engine {
                                int32_t max_stats);
 
   void profile_enable(uint32_t mask);
+  void profile_every(int32_t every);
   int32_t profile_read(rp_kernel_stats* out, int32_t cap);
   void set_kv_policy(int32_t policy);
   void step_trace_enable(int32_t cap);
@@ -269,6 +270,8 @@ class Engine {
   template <typename F> void launch_timed(int cls, double bytes, double flops, F&& launch);
   void prof_harvest();
   uint32_t prof_mask_ = 0;
+  int32_t prof_every_ = 1;                   // time one launch in prof_every_ per class and phase
+  int64_t prof_seen_[RP_K_COUNT][2] = {};    // selected launches since rp_profile_every
   int phase_ = 0;             // 0 prefill, 1 decode
   double sum_ctx_ = 0;        // attended KV tokens of the current forward (decode)
   double sum_ctx_sq_ = 0;     // sum of squared prompt lengths (prefill attention)

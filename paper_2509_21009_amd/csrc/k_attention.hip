@@ -431,14 +431,14 @@ hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s) {
   if (!bf16) {
     if (a.n_rows <= 0) return hipSuccess;
     if (a.hd > 128) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_attn_f32, dim3(a.n_rows, a.n_q), dim3(64), 0, s, a);
+    launch_kernel(k_attn_f32, dim3(a.n_rows, a.n_q), dim3(64), 0, s, a);
     return hipGetLastError();
   }
   if (a.B <= 0 || a.total_splits <= 0) return hipSuccess;
   if (a.n_q / a.n_kv > 16 || a.tokens_per_split % kPageTokens != 0 || !a.split_desc) return hipErrorInvalidValue;
   dim3 grid(a.total_splits, a.n_kv);
-  if (a.hd == 128) hipLaunchKernelGGL(k_attn_decode_bf16<128>, grid, dim3(64), 0, s, a);
-  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_decode_bf16<64>, grid, dim3(64), 0, s, a);
+  if (a.hd == 128) launch_kernel(k_attn_decode_bf16<128>, grid, dim3(64), 0, s, a);
+  else if (a.hd == 64) launch_kernel(k_attn_decode_bf16<64>, grid, dim3(64), 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -446,8 +446,8 @@ hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s) {
 hipError_t launch_attn_merge(const AttnArgs& a, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;
   dim3 grid(a.B, a.n_q);
-  if (a.hd == 128) hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(128 * kMergeGroups), 0, s, a);
-  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_merge<64>, grid, dim3(64 * kMergeGroups), 0, s, a);
+  if (a.hd == 128) launch_kernel(k_attn_merge<128>, grid, dim3(128 * kMergeGroups), 0, s, a);
+  else if (a.hd == 64) launch_kernel(k_attn_merge<64>, grid, dim3(64 * kMergeGroups), 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -456,7 +456,7 @@ hipError_t launch_attn_prefill(int bf16, const AttnArgs& a, hipStream_t s) {
   if (!bf16) {
     if (a.n_rows <= 0) return hipSuccess;
     if (a.hd > 128) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_attn_f32, dim3(a.n_rows, a.n_q), dim3(64), 0, s, a);
+    launch_kernel(k_attn_f32, dim3(a.n_rows, a.n_q), dim3(64), 0, s, a);
     return hipGetLastError();
   }
   if (a.total_items <= 0) return hipSuccess;
@@ -464,8 +464,8 @@ hipError_t launch_attn_prefill(int bf16, const AttnArgs& a, hipStream_t s) {
   if (G > 16) return hipErrorInvalidValue;
   const int tpi = attn_prefill_tokens_per_item(1, G);
   dim3 grid(a.total_items, a.n_kv);
-  if (a.hd == 128) hipLaunchKernelGGL(k_attn_prefill_bf16<128>, grid, dim3(64), 0, s, a, tpi);
-  else if (a.hd == 64) hipLaunchKernelGGL(k_attn_prefill_bf16<64>, grid, dim3(64), 0, s, a, tpi);
+  if (a.hd == 128) launch_kernel(k_attn_prefill_bf16<128>, grid, dim3(64), 0, s, a, tpi);
+  else if (a.hd == 64) launch_kernel(k_attn_prefill_bf16<64>, grid, dim3(64), 0, s, a, tpi);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -8,6 +8,11 @@
 
 namespace rollpack {
 
+LaunchEvents& launch_events() {
+  thread_local LaunchEvents ev;
+  return ev;
+}
+
 namespace {
 
 // Rows are processed by one block of up to 1024 threads, each owning two
@@ -361,7 +366,7 @@ int row_threads(int H) {
 
 template <typename T, int S>
 void launch_add_norm_s(const AddNormArgs& a, int threads, hipStream_t s) {
-  hipLaunchKernelGGL((k_add_rmsnorm<T, S>), dim3(a.M), dim3(threads), 0, s, a);
+  launch_kernel((k_add_rmsnorm<T, S>), dim3(a.M), dim3(threads), 0, s, a);
 }
 
 template <typename T>
@@ -396,22 +401,22 @@ hipError_t launch_rope_t(const RopeArgs& a, hipStream_t s) {
   const int items = (a.n_q + a.n_kv) * (a.hd / 2) + a.n_kv * a.hd;
   dim3 grid(a.M, (items + 255) / 256);
   switch (a.splits) {
-    case 1: hipLaunchKernelGGL((k_rope_append<T, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_rope_append<T, 2>), grid, dim3(256), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_rope_append<T, 3>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_rope_append<T, 4>), grid, dim3(256), 0, s, a); break;
-    case 5: hipLaunchKernelGGL((k_rope_append<T, 5>), grid, dim3(256), 0, s, a); break;
-    case 6: hipLaunchKernelGGL((k_rope_append<T, 6>), grid, dim3(256), 0, s, a); break;
-    case 7: hipLaunchKernelGGL((k_rope_append<T, 7>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((k_rope_append<T, 8>), grid, dim3(256), 0, s, a); break;
-    case 9: hipLaunchKernelGGL((k_rope_append<T, 9>), grid, dim3(256), 0, s, a); break;
-    case 10: hipLaunchKernelGGL((k_rope_append<T, 10>), grid, dim3(256), 0, s, a); break;
-    case 11: hipLaunchKernelGGL((k_rope_append<T, 11>), grid, dim3(256), 0, s, a); break;
-    case 12: hipLaunchKernelGGL((k_rope_append<T, 12>), grid, dim3(256), 0, s, a); break;
-    case 13: hipLaunchKernelGGL((k_rope_append<T, 13>), grid, dim3(256), 0, s, a); break;
-    case 14: hipLaunchKernelGGL((k_rope_append<T, 14>), grid, dim3(256), 0, s, a); break;
-    case 15: hipLaunchKernelGGL((k_rope_append<T, 15>), grid, dim3(256), 0, s, a); break;
-    case 16: hipLaunchKernelGGL((k_rope_append<T, 16>), grid, dim3(256), 0, s, a); break;
+    case 1: launch_kernel((k_rope_append<T, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: launch_kernel((k_rope_append<T, 2>), grid, dim3(256), 0, s, a); break;
+    case 3: launch_kernel((k_rope_append<T, 3>), grid, dim3(256), 0, s, a); break;
+    case 4: launch_kernel((k_rope_append<T, 4>), grid, dim3(256), 0, s, a); break;
+    case 5: launch_kernel((k_rope_append<T, 5>), grid, dim3(256), 0, s, a); break;
+    case 6: launch_kernel((k_rope_append<T, 6>), grid, dim3(256), 0, s, a); break;
+    case 7: launch_kernel((k_rope_append<T, 7>), grid, dim3(256), 0, s, a); break;
+    case 8: launch_kernel((k_rope_append<T, 8>), grid, dim3(256), 0, s, a); break;
+    case 9: launch_kernel((k_rope_append<T, 9>), grid, dim3(256), 0, s, a); break;
+    case 10: launch_kernel((k_rope_append<T, 10>), grid, dim3(256), 0, s, a); break;
+    case 11: launch_kernel((k_rope_append<T, 11>), grid, dim3(256), 0, s, a); break;
+    case 12: launch_kernel((k_rope_append<T, 12>), grid, dim3(256), 0, s, a); break;
+    case 13: launch_kernel((k_rope_append<T, 13>), grid, dim3(256), 0, s, a); break;
+    case 14: launch_kernel((k_rope_append<T, 14>), grid, dim3(256), 0, s, a); break;
+    case 15: launch_kernel((k_rope_append<T, 15>), grid, dim3(256), 0, s, a); break;
+    case 16: launch_kernel((k_rope_append<T, 16>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -422,8 +427,8 @@ hipError_t launch_embed_norm(int bf16, const EmbedArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (a.H % 4 || a.H > 4 * kRowChunks * 1024) return hipErrorInvalidValue;
   const int th = row_threads(a.H);
-  if (bf16) hipLaunchKernelGGL(k_embed_norm<bf16_t>, dim3(a.M), dim3(th), 0, s, a);
-  else hipLaunchKernelGGL(k_embed_norm<float>, dim3(a.M), dim3(th), 0, s, a);
+  if (bf16) launch_kernel(k_embed_norm<bf16_t>, dim3(a.M), dim3(th), 0, s, a);
+  else launch_kernel(k_embed_norm<float>, dim3(a.M), dim3(th), 0, s, a);
   return hipGetLastError();
 }
 
@@ -443,8 +448,8 @@ int sample_chunks(int V) { return (V + kSampleChunk - 1) / kSampleChunk; }
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;
   const int chunks = sample_chunks(a.V);
-  hipLaunchKernelGGL(k_sample_partial, dim3(a.B, chunks), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_sample_final, dim3(a.B), dim3(64), 0, s, a, chunks);
+  launch_kernel(k_sample_partial, dim3(a.B, chunks), dim3(256), 0, s, a);
+  launch_kernel(k_sample_final, dim3(a.B), dim3(64), 0, s, a, chunks);
   return hipGetLastError();
 }
 
@@ -475,14 +480,14 @@ __global__ __launch_bounds__(256) void k_stream_read(const uint4* p, size_t n16)
 
 hipError_t launch_stream_read(const void* buf, size_t bytes, hipStream_t s) {
   if (bytes < 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_stream_read, dim3(kStreamWaves / 4), dim3(256), 0, s, static_cast<const uint4*>(buf), bytes / 16);
+  launch_kernel(k_stream_read, dim3(kStreamWaves / 4), dim3(256), 0, s, static_cast<const uint4*>(buf), bytes / 16);
   return hipGetLastError();
 }
 
 hipError_t launch_gather_rows(const void* src, const int32_t* rows, int n, int H, int esize, void* out,
                               hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gather_rows, dim3(n), dim3(256), 0, s, static_cast<const uint8_t*>(src), rows,
+  launch_kernel(k_gather_rows, dim3(n), dim3(256), 0, s, static_cast<const uint8_t*>(src), rows,
                      H * esize, static_cast<uint8_t*>(out));
   return hipGetLastError();
 }

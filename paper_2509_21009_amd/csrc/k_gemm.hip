@@ -735,7 +735,7 @@ void launch_stream_t(const GemmArgs& a, hipStream_t s) {
   const int n_chunks = a.K / 128;
   const int cps = (n_chunks + a.splits - 1) / a.splits;
   const int blocks = SILU ? a.N / 16 : a.N / (16 * R);
-  hipLaunchKernelGGL((k_gemm_stream<R, MT, SILU>), dim3(blocks, a.splits), dim3(256), 0, s, a, cps);
+  launch_kernel((k_gemm_stream<R, MT, SILU>), dim3(blocks, a.splits), dim3(256), 0, s, a, cps);
 }
 
 template <bool SILU>
@@ -753,7 +753,7 @@ void launch_skinny_t(const GemmArgs& a, hipStream_t s) {
   const int n_chunks = a.K / 128;
   const int cps = (n_chunks + a.splits - 1) / a.splits;
   const int blocks = SILU ? a.N / 64 : a.N / (64 * R);
-  hipLaunchKernelGGL((k_gemm_skinny<R, MT, SILU>), dim3(blocks, a.splits), dim3(256), 0, s, a, cps);
+  launch_kernel((k_gemm_skinny<R, MT, SILU>), dim3(blocks, a.splits), dim3(256), 0, s, a, cps);
 }
 
 template <int R, bool SILU>
@@ -784,7 +784,7 @@ void launch_deep_t(const GemmArgs& a, hipStream_t s) {
   const int ups = (KU + a.splits - 1) / a.splits;
   const int per = SILU ? R / 2 : R;
   const int nb = (a.N / 16 + per - 1) / per;
-  hipLaunchKernelGGL((k_gemm_deep<R, MT, D, SILU>), dim3(nb, a.splits), dim3(256), 0, s, a, ups);
+  launch_kernel((k_gemm_deep<R, MT, D, SILU>), dim3(nb, a.splits), dim3(256), 0, s, a, ups);
 }
 
 // The (R, D) pairs instantiated for each activation tile count MT = ceil(M / 16).
@@ -928,8 +928,8 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
   if (!bf16 || kernel == kKF32) {
     if (bf16 || a.splits != 1) return hipErrorInvalidValue;
     dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
-    if (silu) hipLaunchKernelGGL(k_gemm_f32<true>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_gemm_f32<false>, grid, dim3(256), 0, s, a);
+    if (silu) launch_kernel(k_gemm_f32<true>, grid, dim3(256), 0, s, a);
+    else launch_kernel(k_gemm_f32<false>, grid, dim3(256), 0, s, a);
     return hipGetLastError();
   }
   if (kernel == kKTiled || a.M > 64) {
@@ -951,8 +951,8 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
     dim3 grid(8 * per_xcd, a.splits);
 #define RP_TILED(BM_, BN_)                                                                                   \
     if (bm == BM_ && bn == BN_) {                                                                            \
-      if (silu) hipLaunchKernelGGL((k_gemm_tiled<BM_, BN_, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
-      else hipLaunchKernelGGL((k_gemm_tiled<BM_, BN_, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
+      if (silu) launch_kernel((k_gemm_tiled<BM_, BN_, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
+      else launch_kernel((k_gemm_tiled<BM_, BN_, false>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
     }
     RP_TILED(128, 128) RP_TILED(128, 256) RP_TILED(256, 128) RP_TILED(256, 256)
 #undef RP_TILED

@@ -11,10 +11,33 @@
 //   page table int32 [slot][max_pages_per_seq]
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace rollpack {
+
+// Events that the next kernel launches of this thread stamp from their own
+// dispatch (hipExtLaunchKernelGGL), for timing without marker packets
+// between kernels: the first launch after they are set stamps `start` (and
+// clears it), every launch stamps `stop`, so a launcher of several kernels is
+// timed from the first one's start to the last one's end.  With `stop` null,
+// launches are plain.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();  // this thread's
+
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  LaunchEvents& ev = launch_events();
+  if (ev.stop) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, ev.start, ev.stop, 0, args...);
+    ev.start = nullptr;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+  }
+}
 
 constexpr int kPageTokens = 64;
 

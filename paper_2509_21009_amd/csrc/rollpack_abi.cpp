@@ -238,6 +238,10 @@ rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask) {
   return engine_call(eng, [&](rollpack::Engine* e) { e->profile_enable(class_mask); });
 }
 
+rp_status rp_profile_every(rp_engine* eng, int32_t every) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->profile_every(every); });
+}
+
 rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int32_t* n_out) {
   return engine_call(eng, [&](rollpack::Engine* e) {
     const int32_t n = e->profile_read(out, cap);

@@ -118,6 +118,7 @@ SIGNATURES = {
     "rp_step_trace_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
     "rp_step_trace_read": (ctypes.c_int, [_P, ctypes.POINTER(RpStepRecord), ctypes.c_int32, _I32P]),
     "rp_profile_enable": (ctypes.c_int, [_P, ctypes.c_uint32]),
+    "rp_profile_every": (ctypes.c_int, [_P, ctypes.c_int32]),
     "rp_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(RpKernelStats), ctypes.c_int32, _I32P]),
     "rp_stream_read_gbs": (ctypes.c_int, [_P, ctypes.c_size_t, ctypes.c_int32, _P, ctypes.POINTER(ctypes.c_double)]),
     "rp_last_error": (ctypes.c_char_p, []),
@@ -360,6 +361,11 @@ def rp_profile_enable(eng: int, classes) -> None:
     _check(load_library().rp_profile_enable(eng, mask))
 
 
+def rp_profile_every(eng: int, every: int) -> None:
+    """Time one launch in `every` of each selected class (1: all)."""
+    _check(load_library().rp_profile_every(eng, every))
+
+
 def rp_profile_read(eng: int, cap: int = 64):
     out = (RpKernelStats * cap)()
     n = ctypes.c_int32()
@@ -481,7 +487,8 @@ class Engine:
     def step_trace_read(self, cap: int = 1 << 20):
         return rp_step_trace_read(self.handle, cap)
 
-    def profile(self, classes):
+    def profile(self, classes, every: int = 1):
+        rp_profile_every(self.handle, every)
         rp_profile_enable(self.handle, classes)
 
     def profile_read(self):

@@ -266,6 +266,28 @@ def test_engine_errors_leave_state_unchanged(tiny):
     eng.close()
 
 
+def test_profile_sampling(tiny):
+    """rp_profile_every: one launch in N of a class is timed, from the first, per phase."""
+    s, wd, _ = tiny
+    R = rp()
+    wl = make_workload("tiny")
+    counts = {}
+    for every in (1, 3):
+        eng = _engine(s, wd, 8, 256, 128, 32)
+        eng.profile(["attn", "gemm_gate_up"], every=every)
+        toks, _ = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, 0, 0.0)
+        counts[every] = {(r["kernel"], r["phase"]): r for r in eng.profile_read()}
+        counts[every]["toks"] = toks
+        with pytest.raises(R.RollpackError):
+            eng.profile(["attn"], every=0)
+        eng.close()
+    assert np.array_equal(counts[1]["toks"], counts[3]["toks"])
+    for key in [("attn", "decode"), ("gemm_gate_up", "decode"), ("gemm_gate_up", "prefill")]:
+        full, part = counts[1][key], counts[3][key]
+        assert part["launches"] == (full["launches"] + 2) // 3, key
+        assert part["total_ms"] > 0 and part["bytes"] > 0
+
+
 def test_stream_read_ceiling():
     """rp_stream_read_gbs: a read-only streaming pass over a 1 GiB buffer reports a plausible HBM
     rate, leaves the buffer unchanged, and rejects buffers under 1 MiB."""
