@@ -147,28 +147,50 @@ def measured_stream_gbs(gib: float = 2.0, reps: int = 5) -> float:
     return gbs
 
 
-def prefill_mfma(eng, wl):
-    """MFMA utilisation of the prefill projections, from HIP events on the engine's stream: one untimed
-    prefill of every prompt of the workload (in chunks of max_prefill_tokens), the sequences then
-    aborted.  flops are 2*M*N*K per launch."""
+DECODE_GEMMS = PREFILL_GEMMS + ["gemm_lm_head"]
+FULL_BATCH_DECODE_STEPS = 8
+
+
+def gemm_rates(eng, wl):
+    """MFMA utilisation of the prefill projections and of the decode GEMMs at the round's full batch,
+    from HIP events on the engine's stream: one untimed prefill of every prompt of the workload (in
+    chunks of max_prefill_tokens), then FULL_BATCH_DECODE_STEPS decode steps with every sequence
+    live, the sequences then aborted.  flops are 2*M*N*K per launch, bytes the algorithmic
+    weights + activations + outputs."""
     import torch
     eng.profile(PREFILL_GEMMS)
-    eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, np.maximum(wl.max_new, 2).astype(np.int32),
-                wl.sample_seed, wl.temperature)
+    eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets,
+                np.maximum(wl.max_new, FULL_BATCH_DECODE_STEPS + 2).astype(np.int32), wl.sample_seed, wl.temperature)
     torch.cuda.synchronize()
     prof = [p for p in eng.profile_read() if p["phase"] == "prefill" and p["kernel"] in PREFILL_GEMMS]
+    eng.profile(DECODE_GEMMS)
+    for _ in range(FULL_BATCH_DECODE_STEPS):
+        eng.decode_step()
+    torch.cuda.synchronize()
+    dec = [p for p in eng.profile_read() if p["phase"] == "decode" and p["kernel"] in DECODE_GEMMS]
     eng.profile([])
     eng.abort(wl.seq_ids)
     eng.free_finished()
-    flops = sum(p["flops"] for p in prof)
-    ms = sum(p["total_ms"] for p in prof)
-    if ms <= 0:
-        return None
-    per = {p["kernel"]: round(p["flops"] / (p["total_ms"] * 1e-3) / 1e12, 1) for p in prof}
-    tfs = flops / (ms * 1e-3) / 1e12
-    return {"achieved": round(tfs, 1), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-            "frac": round(tfs / MFMA_BF16_PEAK_TFS, 4), "prompt_tokens": int(wl.prompt_lens().sum()),
-            "per_kernel_tflops": per}
+
+    def rates(ps):
+        flops = sum(p["flops"] for p in ps)
+        ms = sum(p["total_ms"] for p in ps)
+        if ms <= 0:
+            return None
+        tfs = flops / (ms * 1e-3) / 1e12
+        return {"achieved": round(tfs, 1), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(tfs / MFMA_BF16_PEAK_TFS, 4),
+                "hbm_gbs": round(sum(p["bytes"] for p in ps) / (ms * 1e-3) / 1e9, 1),
+                "per_kernel_tflops": {p["kernel"]: round(p["flops"] / (p["total_ms"] * 1e-3) / 1e12, 1) for p in ps}}
+
+    pre = rates(prof)
+    if pre is not None:
+        pre["prompt_tokens"] = int(wl.prompt_lens().sum())
+    full = rates(dec)
+    if full is not None:
+        full["rows"] = int(wl.n)
+        full["steps"] = FULL_BATCH_DECODE_STEPS
+    return pre, full
 
 
 def main():
@@ -284,7 +306,7 @@ def main():
         roof["measured_peak"] = round(stream, 1)
         roof["frac_measured"] = round(roof["achieved"] / stream, 4)
     if shape.dtype == "bf16":
-        out["config"]["prefill_gemm_mfma"] = prefill_mfma(eng, wl)
+        out["config"]["prefill_gemm_mfma"], out["config"]["decode_gemm_full_batch"] = gemm_rates(eng, wl)
     if args.compare_unscheduled and wl.round_id is not None:
         log("running the same sequences as one unscheduled batch")
         _, flat = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, wl.sample_seed,
