@@ -159,12 +159,14 @@ def gemm_rates(eng, wl):
     weights + activations + outputs."""
     import torch
     eng.profile(PREFILL_GEMMS)
-    eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets,
-                np.maximum(wl.max_new, FULL_BATCH_DECODE_STEPS + 2).astype(np.int32), wl.sample_seed, wl.temperature)
+    eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, np.maximum(wl.max_new, 2).astype(np.int32),
+                wl.sample_seed, wl.temperature)
     torch.cuda.synchronize()
     prof = [p for p in eng.profile_read() if p["phase"] == "prefill" and p["kernel"] in PREFILL_GEMMS]
     eng.profile(DECODE_GEMMS)
-    for _ in range(FULL_BATCH_DECODE_STEPS):
+    # steps before the first sequence could finish, so the batch stays whole
+    steps = max(1, min(FULL_BATCH_DECODE_STEPS, int(np.maximum(wl.max_new, 2).min()) - 1))
+    for _ in range(steps):
         eng.decode_step()
     torch.cuda.synchronize()
     dec = [p for p in eng.profile_read() if p["phase"] == "decode" and p["kernel"] in DECODE_GEMMS]
@@ -189,7 +191,7 @@ def gemm_rates(eng, wl):
     full = rates(dec)
     if full is not None:
         full["rows"] = int(wl.n)
-        full["steps"] = FULL_BATCH_DECODE_STEPS
+        full["steps"] = steps
     return pre, full
 
 
