@@ -499,6 +499,7 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     } else {
       aa.B = M; aa.row_slot = m_slot_; aa.row_ctx = m_ctx_; aa.split_off = m_split_off_;
       aa.total_splits = total_splits; aa.tokens_per_split = tps; aa.split_desc = m_split_desc_;
+      aa.max_row_splits = max_row_splits_;
       aa.part_o = sp<float>(plan_.att_o); aa.part_ml = sp<float>(plan_.att_ml);
       launch_timed(RP_K_ATTN, attn_bytes, attn_flops, [&] { return launch_attn_decode(bf16_, aa, s); });
       if (bf16_) {
@@ -759,7 +760,12 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     const int64_t target = decode_split_target(cfg_);
     const int64_t pps = std::max<int64_t>(1, (total_pages + target - 1) / target);
     tps = static_cast<int>(pps * kPageTokens);
-    for (int i = 0; i < B; ++i) total_splits += (ctx_h[i] + tps - 1) / tps;
+    max_row_splits_ = 0;
+    for (int i = 0; i < B; ++i) {
+      const int n = (ctx_h[i] + tps - 1) / tps;
+      total_splits += n;
+      max_row_splits_ = std::max(max_row_splits_, n);
+    }
     if (total_splits > plan_.split_cap) throw RpError(RP_ERR_CAPACITY, "decode split capacity exceeded");
   }
   const size_t desc_at = (7 * static_cast<size_t>(B) + 1 + 3) & ~static_cast<size_t>(3);

@@ -255,6 +255,7 @@ class Engine {
                 *m_item_off_ = nullptr, *m_last_row_ = nullptr, *m_gen_pos_ = nullptr,
                 *m_gen_hist_ = nullptr, *m_gen_slot_ = nullptr, *m_split_desc_ = nullptr;
   std::vector<int32_t> ctx_scratch_;  // decode_step: per-row context lengths
+  int max_row_splits_ = 0;            // decode_step: most attention splits of any row
   std::vector<hipEvent_t> events_;
 
   // per-kernel-class profiling (rp_profile_*)

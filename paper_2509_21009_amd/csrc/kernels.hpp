@@ -123,6 +123,7 @@ struct AttnArgs {
   // decode (one query token per sequence, split over the context):
   int B; const int32_t* row_slot; const int32_t* row_ctx; const int32_t* split_off;
   int total_splits; int tokens_per_split;
+  int max_row_splits;             // most splits of any row (0: unknown); picks the merge kernel
   const int32_t* split_desc;      // [total_splits, 4]: row (+ 2^30 if its only split), first key, end key, slot
   float* part_o; float* part_ml;  // [total_splits * n_kv, 16, hd], [.., 2, 16]
   // prefill (causal over packed prompt chunks):
