@@ -109,6 +109,15 @@ __device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, 
   }
 }
 
+// A 16-byte load marked non-temporal, for the KV cache that a decode step
+// streams exactly once: the caches then do not keep it at the expense of
+// reused lines.  Measured against plain loads, decode attention streams
+// 5.7-5.8 TB/s instead of 5.1-5.2 at 16-64 rows.
+typedef unsigned u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8_t load_bf16x8_nt(const bf16_t* p) {
+  return __builtin_bit_cast(bf16x8_t, __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p)));
+}
+
 template <int HD>
 __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
   constexpr int KS = HD / 32, NB = HD / 16, D = 2;
@@ -154,11 +163,11 @@ __global__ __launch_bounds__(64) void k_attn_decode_bf16(AttnArgs a) {
       // its k-step ks is the contiguous 1 KB run ((2h + tt) * KS + ks) of the page's K block
       const bf16_t* krow = kpool + pb + (((2 * h + tt) * KS) * 16 + c) * 32 + g * 8;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kf[sl][tt][ks] = load_bf16x8(krow + ks * 512);
+      for (int ks = 0; ks < KS; ++ks) kf[sl][tt][ks] = load_bf16x8_nt(krow + ks * 512);
     }
     const bf16_t* vh = vpool + pb + h * HD * 32;
 #pragma unroll
-    for (int blk = 0; blk < NB; ++blk) vf[sl][blk] = load_bf16x8(vh + (blk * 16 + c) * 32 + 8 * g);
+    for (int blk = 0; blk < NB; ++blk) vf[sl][blk] = load_bf16x8_nt(vh + (blk * 16 + c) * 32 + 8 * g);
   };
 
   f32x4_t o[NB];
