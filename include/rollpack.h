@@ -394,8 +394,8 @@ rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int
  * peak (the roofline of the memory-bound decode kernels): streams the
  * caller's device buffer dev_buf (bytes >= 1 MiB, 16-byte aligned; its
  * contents are read, never written) reps times with a read-only kernel in
- * which each of 2048 waves walks its own contiguous share with 8 one-KB loads
- * in flight, on hip_stream, and returns
+ * which each of 2048 waves walks its own contiguous share with 8 one-KB
+ * non-temporal loads in flight, on hip_stream, and returns
  * the fastest pass in GB/s (1e9 bytes/s) through gbs_out.  Blocks the calling
  * thread; needs no engine and allocates no device memory.  A buffer larger
  * than the 256 MB last-level cache measures HBM.  Errors: RP_ERR_INVALID_ARG
