@@ -196,6 +196,36 @@ def test_long_context_many_splits():
     assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, r
 
 
+@pytest.mark.parametrize("plen,kernel", [
+    ([450, 300, 200, 100, 64, 30, 10, 3], "one-wave merge, up to 8 splits"),
+    ([3800, 1900, 700, 300, 130, 65, 20, 5], "one-wave merge, up to 64 splits"),
+    ([4150, 1900, 700, 300, 130, 65, 20, 5], "1024-thread merge (a row of 65 splits)"),
+])
+def test_split_merge_kernels_at_eight_rows(plen, kernel):
+    """Eight decode rows of one-page to 65-page contexts, one split per page: single-split rows
+    are written by the decode kernel, the others are merged, from eight rows up by the one-wave
+    kernel while no row has more than 64 splits, else by the 1024-thread kernel.  Three rows
+    (the longest, a middle one, a single-split one) are compared with the oracle."""
+    s = truncated(SHAPES["qwen2.5-0.5b"], 1, vocab=2048)
+    s = dataclasses.replace(s, tied=False)
+    wd = make_weights(s, seed=8, device=DEV)
+    w64 = weights_to_numpy(wd)
+    rng = np.random.default_rng(22)
+    prompts = [rng.integers(0, s.vocab, size=p).astype(np.int32) for p in plen]
+    offs = np.zeros(len(plen) + 1, np.int64)
+    offs[1:] = np.cumsum(plen)
+    from workloads.gen import Workload
+    n = len(plen)
+    wl = Workload("merge", s, np.arange(40, 40 + n, dtype=np.int64), np.concatenate(prompts), offs,
+                  np.full(n, 3, np.int32), np.arange(n, dtype=np.int32), 1.0, 6)
+    log(f"split merge at 8 rows: {kernel}")
+    eng = _engine(s, wd, n, 4200, 4224, n * 67)
+    r = teacher_forced_parity(eng, s, w64, wl, 3, 2e-2, 1.0, 6, check=[0, 2, n - 1])
+    eng.close()
+    log(f"{kernel}: {r}")
+    assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, r
+
+
 def test_page_boundaries_chunked_prefill_and_short_sequences():
     """Prompts of 1, 63, 64, 65 and 130 tokens, max_new 1 and 70 (decode crosses pages),
     prefill split into chunks of at most 140 tokens."""
