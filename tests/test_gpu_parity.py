@@ -304,7 +304,7 @@ def test_profile_sampling(tiny):
     counts = {}
     for every in (1, 3):
         eng = _engine(s, wd, 8, 256, 128, 32)
-        eng.profile(["attn", "gemm_gate_up"], every=every)
+        eng.profile(["attn", "gemm_gate_up", "sample"], every=every)
         toks, _ = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, 0, 0.0)
         counts[every] = {(r["kernel"], r["phase"]): r for r in eng.profile_read()}
         counts[every]["toks"] = toks
@@ -312,7 +312,8 @@ def test_profile_sampling(tiny):
             eng.profile(["attn"], every=0)
         eng.close()
     assert np.array_equal(counts[1]["toks"], counts[3]["toks"])
-    for key in [("attn", "decode"), ("gemm_gate_up", "decode"), ("gemm_gate_up", "prefill")]:
+    # sampling launches two kernels: its events run from the first one's start to the last one's end
+    for key in [("attn", "decode"), ("gemm_gate_up", "decode"), ("gemm_gate_up", "prefill"), ("sample", "decode")]:
         full, part = counts[1][key], counts[3][key]
         assert part["launches"] == (full["launches"] + 2) // 3, key
         assert part["total_ms"] > 0 and part["bytes"] > 0
