@@ -205,6 +205,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-every", type=int, default=8,
                     help="time one launch in N of the roofline kernel inside the timed rounds (1: all)")
+    ap.add_argument("--class-rates", action="store_true",
+                    help="time every kernel class (one launch in --profile-every) inside the timed rounds and report "
+                         "each class's decode rate in config.decode_class_rates (slows the rounds by a few percent)")
     ap.add_argument("--max-prefill-tokens", type=int, default=16384)
     ap.add_argument("--step-trace", default=None, metavar="PATH",
                     help="after the timed steps, run one more (untimed) round with the per-step trace on and write "
@@ -249,7 +252,7 @@ def main():
         t0 = time.perf_counter()
         call()
         log(f"warmup step {i + 1}/{args.warmup} done in {time.perf_counter() - t0:.1f} s")
-    eng.profile([args.kernel], every=args.profile_every)
+    eng.profile(list(rp.KERNEL_CLASSES) if args.class_rates else [args.kernel], every=args.profile_every)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     all_stats = []
@@ -300,6 +303,12 @@ def main():
                    "rounds": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in s.items()} for s in last]},
         "roofline": roof,
     }
+    if args.class_rates:
+        out["config"]["decode_class_rates"] = {
+            p["kernel"]: {"timed_launches": p["launches"], "avg_us": round(p["total_ms"] * 1e3 / p["launches"], 2),
+                          "gbs": round(p["bytes"] / (p["total_ms"] * 1e-3) / 1e9, 1),
+                          "tflops": round(p["flops"] / (p["total_ms"] * 1e-3) / 1e12, 1)}
+            for p in prof if p["phase"] == "decode" and p["launches"] > 0}
     if len(all_stats) > 1:
         out["config"]["round_makespan_median_s"] = round(float(np.median(
             [sum(s_["makespan_ms"] for s_ in st) / 1e3 for st in all_stats])), 3)
