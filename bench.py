@@ -1,11 +1,17 @@
 #!/usr/bin/env python3
 """Rollout benchmark on one MI355X.
 
-One "step" is one whole rollout round of the workload through the C ABI
-(rp_rollout_generate): round formation, paged-KV admission, chunked prefill,
-decode steps until the longest response is done with finished sequences
-freed as they go, seeded sampling and round metrics.  Inputs (weights,
-prompts) are resident in HBM / host memory before the timed region.
+A "step" is one decode step of a rollout round.  The timed region runs whole
+rounds of the workload through the C ABI (rp_rollout_generate): paged-KV
+admission, chunked prefill, decode steps until the longest response is done
+with finished sequences freed as they go, seeded sampling and the round
+metrics.  Rounds repeat until at least --steps decode steps have been timed
+(one round of the default workload is 16,383 decode steps, about a minute and
+a half), and `steps` in the output line counts the decode steps actually
+timed.  Warm-up: every sequence of the workload is prefilled, --warmup decode
+steps run at the full batch, and the sequences are aborted, all untimed.
+Inputs (weights, prompts) are resident in HBM / host memory before the timed
+region.
 
 Default workload: Qwen2.5-7B shape, bf16 random weights, the long round of 64
 sequences with long-tail forced response lengths (lognormal, median 4096,
@@ -64,53 +70,108 @@ def decode_bytes_model(shape, prompt_lens, max_new):
     return total, steps
 
 
+EMBED_ROWS = 1024
+
+
+def live_rows_per_step(wl):
+    """Rows (live sequences) of every decode step of the workload's rounds, in order."""
+    rounds = [np.arange(wl.n)] if wl.round_id is None else [np.flatnonzero(wl.round_id == r)
+                                                             for r in sorted(set(wl.round_id.tolist()))]
+    rows = []
+    for idx in rounds:
+        L = np.sort(np.asarray(wl.max_new[idx], np.int64))
+        j = np.arange(1, int(L[-1]))
+        rows.append(len(L) - np.searchsorted(L, j, side="right"))
+    return np.concatenate(rows)
+
+
 def cpu_baseline(weights, shape, wl):
     """Time the oracle on a bounded sample and scale it to generated tokens/s.
 
-    Sample: one sequence of the workload (its real prompt), the first layer
-    plus the LM head, prefill then 4 decode steps; the per-layer share of the
-    times is scaled to all layers.  The oracle decodes one sequence at a time,
-    so its rate over the workload is sum(L) / sum(prefill_i + L_i * step).
+    Sample: full-batch decode steps of the oracle (oracle.model.decode_step_batch:
+    one step for B sequences, [B, H] products) through the first layer plus the
+    LM head, at B = every sequence of the workload, 64, 8 and 1; the caches hold
+    the rows' real prompt lengths of random keys and values (the step's work
+    depends on their lengths only).  One prefill of the shortest prompt through
+    the first layer (KVState.step, which also computes the LM head of every
+    prompt position) is timed too.  The per-layer share is scaled to all layers,
+    and the round is extrapolated step by step with each step's live row count
+    (times interpolated linearly in B between the measured batches).
     """
     from threadpoolctl import threadpool_info
 
     from oracle import model as om
     from workloads import truncated, weights_to_numpy
 
-    sub = {"embed": weights["embed"], "final_norm": weights["final_norm"], "lm_head": weights["lm_head"],
+    t_sample0 = time.perf_counter()
+    # An untied model reads the embedding only at the sample's token ids: the sample converts its first
+    # EMBED_ROWS rows and takes token ids below that (the work does not depend on the ids).
+    n_emb = shape.vocab if weights["lm_head"] is None else min(EMBED_ROWS, shape.vocab)
+    sub = {"embed": weights["embed"][:n_emb], "final_norm": weights["final_norm"], "lm_head": weights["lm_head"],
            "layers": weights["layers"][:1]}
     w64 = weights_to_numpy(sub)
+    t_convert = time.perf_counter() - t_sample0
     s1 = truncated(shape, 1)
-    prompt = wl.prompt(0)
+    plens = wl.prompt_lens()
+    rng = np.random.default_rng(0)
+
+    def states_for(idx):
+        sts = []
+        for i in idx:
+            st = om.KVState(s1)
+            n = int(plens[i])
+            st.k[0] = rng.standard_normal((n, shape.n_kv, shape.head_dim)) * 0.5
+            st.v[0] = rng.standard_normal((n, shape.n_kv, shape.head_dim)) * 0.5
+            st.length = n
+            sts.append(st)
+        return sts
+
+    def best_of(reps, fn):
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return min(ts)
+
+    batches = sorted({b for b in (wl.n, 64, 8, 1) if b <= wl.n})
+    om.decode_step_batch(w64, states_for([0]), [0])  # first call: thread pools and first touch, untimed
+    t_full, t_lm = {}, {}
+    for B in batches:
+        idx = np.arange(B)
+        sts = states_for(idx)
+        toks = np.array([wl.prompt(i)[-1] for i in idx]) % n_emb
+        t_step1 = best_of(2, lambda: om.decode_step_batch(w64, sts, toks))
+        x = rng.standard_normal((B, shape.hidden))
+        t_lm[B] = best_of(2, lambda: om.lm_head(w64, x, s1))
+        t_full[B] = shape.layers * max(t_step1 - t_lm[B], 0.0) + t_lm[B]
+    bs = np.array(batches, np.float64)
+    tf = np.array([t_full[b] for b in batches])
+    decode_t = float(np.sum(np.interp(live_rows_per_step(wl), bs, tf)))
+    # prefill of the shortest prompt through layer 0 (with the oracle's LM head over every position)
+    i0 = int(np.argmin(plens))
     st = om.KVState(s1)
     t0 = time.perf_counter()
-    logits = st.step(w64, prompt)[-1]
-    t_prefill_1 = time.perf_counter() - t0
-    tok = int(np.argmax(logits))
-    times = []
-    for _ in range(4):
-        t0 = time.perf_counter()
-        tok = int(np.argmax(st.step(w64, [tok])[-1]))
-        times.append(time.perf_counter() - t0)
-    t_dec_1 = float(np.median(times))
-    x = np.random.default_rng(0).standard_normal((1, shape.hidden))
-    lm = []
-    for _ in range(3):
-        t0 = time.perf_counter()
-        om.lm_head(w64, x, s1)
-        lm.append(time.perf_counter() - t0)
-    t_lm = float(np.median(lm))
-    t_step = shape.layers * max(t_dec_1 - t_lm, 0.0) + t_lm
-    t_pre_per_tok = shape.layers * max(t_prefill_1 - t_lm, 0.0) / len(prompt)
-    plens = wl.prompt_lens()
-    total_t = float(np.sum(plens * t_pre_per_tok + t_lm + (wl.max_new - 1) * t_step))
-    rate = float(np.sum(wl.max_new)) / total_t
+    st.step(w64, wl.prompt(i0) % n_emb)
+    t_pre = time.perf_counter() - t0
+    p0 = int(plens[i0])
+    t0 = time.perf_counter()
+    om.lm_head(w64, rng.standard_normal((p0, shape.hidden)), s1)
+    t_pre_lm = time.perf_counter() - t0
+    per_tok = (shape.layers * max(t_pre - t_pre_lm, 0.0) + t_pre_lm) / p0
+    prefill_t = float(np.sum(plens)) * per_tok
+    total_t = decode_t + prefill_t
+    gen = int(np.sum(wl.max_new))
     threads = sum(int(i.get("num_threads", 0)) for i in threadpool_info() if i.get("user_api") == "blas") or 1
-    return {"value": rate, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": (f"fp64 numpy oracle, sequence 0 of the workload (prompt {len(prompt)} tokens): prefill and "
-                       f"4 decode steps through layer 0 + LM head, per-layer time x{shape.layers} layers, "
-                       f"extrapolated over all {wl.n} sequences ({int(np.sum(wl.max_new))} tokens); "
-                       f"measured step {t_step:.2f} s/token, host cpus {len(os.sched_getaffinity(0))}"),
+    return {"value": round(gen / total_t, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"fp64 numpy oracle (oracle.model.decode_step_batch), full-batch decode steps through layer 0 "
+                       f"+ LM head at B = {batches} (s/step scaled to {shape.layers} layers: "
+                       + ", ".join(f"B={b}: {t_full[b]:.2f}" for b in batches)
+                       + f"), plus a {p0}-token prefill through layer 0; extrapolated over the "
+                       f"{len(live_rows_per_step(wl))} decode steps of the workload ({gen} tokens) with each step's "
+                       f"live rows: decode {decode_t:.0f} s + prefill {prefill_t:.0f} s; host cpus "
+                       f"{len(os.sched_getaffinity(0))}; sample took {time.perf_counter() - t_sample0:.1f} s, of which "
+                       f"{t_convert:.1f} s converting the sampled weights to fp64"),
             "extrapolated": True}
 
 
@@ -195,14 +256,30 @@ def gemm_rates(eng, wl):
     return pre, full
 
 
+def warmup_steps(eng, wl, n_steps):
+    """Untimed: prefill every sequence of the workload, run n_steps decode steps at the full
+    batch, then abort the sequences."""
+    if n_steps <= 0:
+        return
+    eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, np.maximum(wl.max_new, 2).astype(np.int32),
+                wl.sample_seed, wl.temperature)
+    for _ in range(n_steps):
+        eng.decode_step()
+    eng.abort(wl.seq_ids)
+    eng.free_finished()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1,
+                    help="decode steps to time, at least: whole rounds run until this many have been timed")
+    ap.add_argument("--warmup", type=int, default=4, help="untimed decode steps at the full batch first")
     ap.add_argument("--workload", default="7b-long", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--kernel", default="gemm_gate_up", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-rates", action="store_true",
+                    help="skip the MFMA-utilisation pass (prefill projections, decode GEMMs at the full batch)")
     ap.add_argument("--profile-every", type=int, default=8,
                     help="time one launch in N of the roofline kernel inside the timed rounds (1: all)")
     ap.add_argument("--class-rates", action="store_true",
@@ -222,6 +299,7 @@ def main():
               "rollout sequences shard across GPUs as independent engines, which this build does not run.",
               file=sys.stderr)
         sys.exit(2)
+    t_start = time.perf_counter()
 
     import torch
 
@@ -248,25 +326,28 @@ def main():
                     max_context=need_ctx, kv_pages=pages)
     call = lambda: eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, wl.sample_seed,  # noqa
                                wl.temperature, wl.round_id)
-    for i in range(args.warmup):
-        t0 = time.perf_counter()
-        call()
-        log(f"warmup step {i + 1}/{args.warmup} done in {time.perf_counter() - t0:.1f} s")
+    t0 = time.perf_counter()
+    warmup_steps(eng, wl, args.warmup)
+    torch.cuda.synchronize()
+    log(f"warm-up: prefill + {args.warmup} decode steps at {wl.n} rows in {time.perf_counter() - t0:.1f} s")
     eng.profile(list(rp.KERNEL_CLASSES) if args.class_rates else [args.kernel], every=args.profile_every)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     all_stats = []
-    for i in range(args.steps):
+    timed_steps = 0
+    while timed_steps < max(args.steps, 1):
         _, stats = call()
         all_stats.append(stats)
-        log(f"timed step {i + 1}/{args.steps}: " + ", ".join(
-            f"round {s['round_id']}: {s['makespan_ms'] / 1e3:.2f} s" for s in stats))
+        timed_steps += sum(int(s["decode_steps"]) for s in stats)
+        log(f"timed round set {len(all_stats)}: " + ", ".join(
+            f"round {s['round_id']}: {s['makespan_ms'] / 1e3:.2f} s, {s['decode_steps']} decode steps" for s in stats))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     prof = eng.profile_read()
     eng.profile([])
 
-    gen_tokens = int(wl.max_new.sum()) * args.steps
+    n_sets = len(all_stats)
+    gen_tokens = int(wl.max_new.sum()) * n_sets
     value = gen_tokens / elapsed
     last = all_stats[-1]
     decode_s = sum(s["decode_ms"] for s in last) / 1e3
@@ -291,12 +372,14 @@ def main():
                 "avg_launch_us": round(avg_ms * 1e3, 2),
                 "algorithmic_bytes_per_launch": bytes_per}
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 1), "higher_is_better": True,
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": timed_steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / timed_steps, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "sequences": wl.n,
-                   "generated_tokens_per_step": int(wl.max_new.sum()),
-                   "prompt_tokens_per_step": int(plens.sum()),
+                   "step": "one decode step; the timed region is whole rounds (prefill, decode, sampling, freeing)",
+                   "requested_steps": args.steps, "timed_round_sets": n_sets, "timed_s": round(elapsed, 3),
+                   "generated_tokens_per_round_set": int(wl.max_new.sum()),
+                   "prompt_tokens_per_round_set": int(plens.sum()),
                    "makespan_s": round(makespan_s, 3), "decode_s": round(decode_s, 3),
                    "decode_tokens_per_s": round(int(wl.max_new.sum()) / max(decode_s, 1e-9), 1),
                    "decode_hbm_frac": round(dec_bytes / max(decode_s, 1e-9) / (HBM_PEAK_GBS * 1e9), 4),
@@ -309,15 +392,18 @@ def main():
                           "gbs": round(p["bytes"] / (p["total_ms"] * 1e-3) / 1e9, 1),
                           "tflops": round(p["flops"] / (p["total_ms"] * 1e-3) / 1e12, 1)}
             for p in prof if p["phase"] == "decode" and p["launches"] > 0}
-    if len(all_stats) > 1:
+    if n_sets > 1:
         out["config"]["round_makespan_median_s"] = round(float(np.median(
             [sum(s_["makespan_ms"] for s_ in st) / 1e3 for st in all_stats])), 3)
+    log(f"timed: {timed_steps} decode steps in {elapsed:.2f} s, {value:.1f} tokens/s")
     if roof is not None:
         stream = measured_stream_gbs()
         roof["measured_peak"] = round(stream, 1)
         roof["frac_measured"] = round(roof["achieved"] / stream, 4)
-    if shape.dtype == "bf16":
+    if shape.dtype == "bf16" and not args.no_gemm_rates:
+        t0 = time.perf_counter()
         out["config"]["prefill_gemm_mfma"], out["config"]["decode_gemm_full_batch"] = gemm_rates(eng, wl)
+        log(f"GEMM rate pass in {time.perf_counter() - t0:.1f} s")
     if args.compare_unscheduled and wl.round_id is not None:
         log("running the same sequences as one unscheduled batch")
         _, flat = eng.rollout(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, wl.max_new, wl.sample_seed,
@@ -342,10 +428,13 @@ def main():
                        "records": [[int(r["kind"]), int(r["round_id"]), int(r["rows"]), int(r["sum_ctx"]),
                                     round(float(r["ms"]), 5)] for r in rec]}, f)
         log(f"step trace: {len(rec)} records written to {args.step_trace}")
+    eng.close()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
+        t0 = time.perf_counter()
         out["cpu_baseline"] = cpu_baseline(weights, shape, wl)
-    eng.close()
+        log(f"CPU oracle sample in {time.perf_counter() - t0:.1f} s")
+    out["config"]["process_s"] = round(time.perf_counter() - t_start, 1)
     print(json.dumps(out), flush=True)
 
 

@@ -195,3 +195,35 @@ def teacher_forced_logits(w: dict, shape, prompt, response, rnd=None) -> np.ndar
     """Logits that predict response[j] given prompt + response[:j], rows j = 0..L-1."""
     seq = np.concatenate([np.asarray(prompt), np.asarray(response)[:-1]])
     return forward_full(w, shape, seq, rnd)[len(prompt) - 1:]
+
+
+def decode_step_batch(w: dict, states, tokens) -> np.ndarray:
+    """One decode step for several sequences at once: logits [B, V].
+
+    Sequence b appends tokens[b] at its own position states[b].length.  Every
+    projection, norm and MLP acts on each row independently, so they run on
+    the whole batch as [B, H] products; RoPE uses each row's position and the
+    attention of row b reads only its own cache.  Row b equals
+    ``states[b].step(w, [tokens[b]])[-1]`` (the definition, batched).
+    """
+    shape = states[0].shape
+    rnd = states[0].rnd
+    r = rnd or _id
+    tokens = np.asarray(tokens)
+    pos = np.array([st.length for st in states])
+    cos, sin = rope_cos_sin(pos, shape.head_dim, shape.theta)
+    x = w["embed"][tokens].astype(np.float64)
+    for li, layer in enumerate(w["layers"]):
+        h = r(rmsnorm(x, layer["attn_norm"], shape.eps))
+        q, k, v = _qkv(layer, h, shape)
+        q, k, v = r(apply_rope(q, cos, sin)), r(apply_rope(k, cos, sin)), r(v)
+        a = np.empty_like(q)
+        for b, st in enumerate(states):
+            st.k[li] = np.concatenate([st.k[li], k[b:b + 1]])
+            st.v[li] = np.concatenate([st.v[li], v[b:b + 1]])
+            a[b] = attention(q[b:b + 1], st.k[li], st.v[li], pos[b:b + 1], np.arange(pos[b] + 1), rnd)[0]
+        x = x + r(a.reshape(len(states), -1)) @ layer["wo"].T
+        x = x + _mlp(layer, x, shape, r)
+    for st in states:
+        st.length += 1
+    return lm_head(w, x, shape, rnd)

@@ -209,3 +209,24 @@ def test_rounding_diagnostic_reduces_to_plain_oracle(tiny):
 def test_truncated_shape_keeps_layer_dims():
     s = truncated(SHAPES["qwen2.5-7b"], 2)
     assert s.layers == 2 and s.hidden == 3584 and s.group == 7
+
+
+def test_batched_decode_step_equals_per_sequence_steps(tiny):
+    """decode_step_batch against brute force: each row recomputed from scratch
+    over its whole sequence (prompts of different lengths, so rows sit at
+    different positions and attend to different cache lengths)."""
+    s, w = tiny
+    rng = np.random.default_rng(11)
+    prompts = [rng.integers(0, s.vocab, size=n) for n in (5, 17, 33, 1)]
+    states = [om.KVState(s) for _ in prompts]
+    for st, p in zip(states, prompts):
+        st.step(w, p)
+    seqs = [list(p) for p in prompts]
+    for _ in range(3):
+        nxt = rng.integers(0, s.vocab, size=len(prompts))
+        got = om.decode_step_batch(w, states, nxt)
+        for b in range(len(prompts)):
+            seqs[b].append(int(nxt[b]))
+            ref = om.forward_full(w, s, np.array(seqs[b]))[-1]
+            assert np.max(np.abs(got[b] - ref)) / np.max(np.abs(ref)) < 1e-12
+    assert [st.length for st in states] == [len(q) for q in seqs]
