@@ -130,15 +130,20 @@ typedef struct rp_round_stats {
 } rp_round_stats;
 
 /* Bytes of the caller-provided KV pool and scratch workspace for this model
- * and these limits.  kv_bytes covers limits->kv_pages pages; both are
+ * and these limits.  Paper: the KV cache is the memory that long responses
+ * fill and whose shortage causes preemptions (section 4.2); the pool is sized
+ * here by the caller, in 64-token pages.  kv_bytes covers limits->kv_pages pages; both are
  * multiples of 256. */
 rp_status rp_workspace_size(const rp_model_config* cfg, const rp_engine_limits* limits,
                             size_t* kv_bytes, size_t* scratch_bytes);
 
-/* Bytes of KV cache one token occupies (all layers, K and V). */
+/* Bytes of KV cache one token occupies (all layers, K and V); the unit of the
+ * KV footprint projected per request (section 4.4). */
 rp_status rp_kv_bytes_per_token(const rp_model_config* cfg, size_t* bytes);
 
-/* Create an engine over caller-owned device memory.  kv_ws/scratch_ws must
+/* Create an engine over caller-owned device memory: one rollout instance
+ * holding the actor model's weights (section 2.1) that requests are added to
+ * and aborted from (section 5, add_request / abort_request).  kv_ws/scratch_ws must
  * be at least the sizes rp_workspace_size returns and 256-byte aligned;
  * hip_stream is a hipStream_t (NULL = default stream).  The weights are not
  * copied; their device memory must outlive the engine. */
@@ -150,7 +155,9 @@ rp_status rp_engine_create(const rp_model_config* cfg, const rp_weights* weights
 void rp_engine_destroy(rp_engine* eng);
 
 /* Admit n sequences and run their prompts through the model (prefill), then
- * sample each sequence's first response token.
+ * sample each sequence's first response token.  Paper: the actor is given
+ * prompts and generates responses for them (section 2.1); admitting a request
+ * is section 5's add_request.
  *   seq_ids         host [n], new unique ids
  *   prompt_tokens   host, all prompts concatenated (CSR), ids in [0, V)
  *   prompt_offsets  host [n+1], prompt i is tokens [off[i], off[i+1]), length >= 1
@@ -170,7 +177,8 @@ rp_status rp_prefill(rp_engine* eng, int32_t n, const int64_t* seq_ids,
                      float* logits_out, int32_t* first_tokens_out);
 
 /* One decode step for every live, unfinished sequence ("row"), rows in
- * admission order.  Each row feeds its last sampled token (or
+ * admission order: the autoregressive generation step of rollout (section
+ * 2.1), memory-bound at these batch sizes (section 2.2).  Each row feeds its last sampled token (or
  * forced_tokens[row], teacher forcing: the input changes, the sampled history
  * does not), appends its K/V, and samples its next token.
  *   forced_tokens   HOST [n_active] or NULL
@@ -189,27 +197,31 @@ rp_status rp_decode_step(rp_engine* eng, const int32_t* forced_tokens, float* lo
                          int64_t* row_ids_out, int32_t* n_active_out);
 
 /* Release the KV pages and slots of finished sequences and report their ids
- * (host [cap]).  The tokens of a released sequence are no longer available. */
+ * (host [cap]).  Paper: finished requests leave the running set, so the
+ * batch shrinks as short responses complete (section 2.2; Algorithm 1's
+ * generate returns the finished requests).  The tokens of a released sequence are no longer available. */
 rp_status rp_free_finished(rp_engine* eng, int64_t* finished_ids_out, int32_t cap,
                            int32_t* n_finished_out);
 
-/* Stop live (or preempted) sequences now (speculative abort, section 3) and
- * release them. */
+/* Stop live (or preempted) sequences now and release them: the speculative
+ * abort of tail batching (section 3), section 5's abort_request. */
 rp_status rp_abort(rp_engine* eng, int32_t n, const int64_t* seq_ids);
 
 /* Copy the generated tokens of a live (or preempted) sequence to host out
- * [cap]; len_out gets the number generated so far.  Synchronises the stream. */
+ * [cap] (the responses rollout hands to the reward stage, section 2.1); len_out gets the number generated so far.  Synchronises the stream. */
 rp_status rp_get_tokens(rp_engine* eng, int64_t seq_id, int32_t* out, int32_t cap,
                         int32_t* len_out);
 
 /* The same for the log-probability of each generated token under the
- * distribution it was sampled from, log softmax(logits / T)[token]
+ * distribution it was sampled from (the training stage of section 2.1
+ * updates the actor from its responses), log softmax(logits / T)[token]
  * (T = 1 for greedy sequences), as RL training needs for its importance
  * ratios; fp32, from the logits the step computed. */
 rp_status rp_get_logprobs(rp_engine* eng, int64_t seq_id, float* out, int32_t cap,
                           int32_t* len_out);
 
-/* End-of-sequence token (-1, the default: none).  A sequence that samples it
+/* End-of-sequence token (-1, the default: none); response lengths are what
+ * the model decides, long-tailed (section 2.2).  A sequence that samples it
  * stops there, the token included, before max_new_tokens.  The engine reads
  * each step's sampled tokens two steps later, so that it never waits on the
  * step just launched: a stopped sequence may take part in one more step,
@@ -219,7 +231,9 @@ rp_status rp_get_logprobs(rp_engine* eng, int64_t seq_id, float* out, int32_t ca
  * position.  The engine must have no live sequences (RP_ERR_BAD_STATE). */
 rp_status rp_set_eos(rp_engine* eng, int32_t eos_token);
 
-/* Whole-batch rollout: generate max_new_tokens[i] tokens for each of n
+/* Whole-batch rollout on an engine: the rollout stage of section 2.1 (P0
+ * prompts x R0 responses, one sequence each) run as the rounds of section 3
+ * when round_ids are given.  Generate max_new_tokens[i] tokens for each of n
  * sequences, round by round (rounds in increasing round_ids order; NULL =
  * one round).  Within a round all sequences are admitted together (prefill
  * in chunks), then decoded until the last one finishes, freeing KV pages as
@@ -243,6 +257,54 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
                               float* resp_logprobs_out, int32_t* resp_len_out,
                               rp_round_stats* stats_out, int32_t max_stats,
                               int32_t* n_rounds_out);
+
+/* How rp_generate groups its sequences into rounds. */
+typedef enum rp_schedule_mode {
+  RP_SCHEDULE_NONE = 0,           /* every sequence in one batch (round_ids must be NULL) */
+  RP_SCHEDULE_ROUNDS = 1,         /* the caller's rounds, round_ids[i] per sequence */
+  RP_SCHEDULE_TAIL_BATCHING = 2   /* tail batching run online (section 3), with rp_tail_params */
+} rp_schedule_mode;
+
+/* Tail-batching parameters (section 3; eta_p and eta_r vary separately in
+ * section 6.3).  r_spec = ceil(eta_r * R0) candidate responses per prompt. */
+typedef struct rp_tail_params {
+  int32_t P0;       /* prompts kept per short round */
+  int32_t R0;       /* responses kept per prompt */
+  int32_t r_spec;   /* responses launched per prompt */
+  float eta_p;      /* prompt speculation factor, >= 1 */
+  float eta_r;      /* response speculation factor, >= 1 */
+} rp_tail_params;
+
+/* One-shot rollout in the form of the problem statement (section 2.1: the
+ * actor is given P0 prompts and produces R0 responses for each; Algorithm 1's
+ * LLM.generate returns the finished requests): create an engine over the
+ * caller's workspaces, generate every response, destroy the engine.
+ *   cfg, weights, limits, kv_ws, kv_bytes, scratch_ws, scratch_bytes,
+ *   hip_stream      as rp_engine_create (the workspaces are free again when
+ *                   the call returns)
+ *   n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
+ *   temperature     as rp_rollout_generate; under RP_SCHEDULE_TAIL_BATCHING
+ *                   as rp_rollout_tail_batched: n = n_prompts * tail->r_spec,
+ *                   prompt_offsets has n_prompts + 1 entries (CSR over prompts)
+ *   schedule_mode   rp_schedule_mode
+ *   round_ids       host [n] under RP_SCHEDULE_ROUNDS, else NULL
+ *   tail            host, under RP_SCHEDULE_TAIL_BATCHING, else NULL
+ *   resp_tokens_out, resp_logprobs_out (nullable), resp_len_out (nullable,
+ *                   except under RP_SCHEDULE_TAIL_BATCHING), stats_out
+ *                   (nullable), max_stats, n_rounds_out (nullable): as the
+ *                   engine call of the mode
+ *   kept_out        host [n] or NULL: 1 for the responses tail batching keeps
+ *                   (every response under the other modes)
+ * Errors: those of rp_engine_create and of the engine call; no device memory
+ * is allocated and nothing is left behind on failure. */
+rp_status rp_generate(const rp_model_config* cfg, const rp_weights* weights, const rp_engine_limits* limits,
+                      void* kv_ws, size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, void* hip_stream,
+                      int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
+                      const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed,
+                      float temperature, int32_t schedule_mode, const int32_t* round_ids,
+                      const rp_tail_params* tail, int32_t* resp_tokens_out, float* resp_logprobs_out,
+                      int32_t* resp_len_out, int32_t* kept_out, rp_round_stats* stats_out, int32_t max_stats,
+                      int32_t* n_rounds_out);
 
 /* Tail batching run online on the engine (section 3).  n_prompts prompts,
  * submitted in order, each with r_spec = ceil(eta_r * R0) candidate responses;
@@ -331,11 +393,14 @@ typedef enum rp_kv_policy {
                            later resume it by recomputing its KV from its tokens */
 } rp_kv_policy;
 
-/* Set the KV page policy (rp_kv_policy).  The engine must have no live or
+/* Set the KV page policy (rp_kv_policy): reservation, or pages on demand with
+ * preemption under KV pressure (section 4.2) and resume by recomputation
+ * (the recomputation-based migration of section 5).  The engine must have no live or
  * preempted sequences (RP_ERR_BAD_STATE). */
 rp_status rp_set_kv_policy(rp_engine* eng, int32_t policy);
 
-/* Pool and scheduler state; every output is nullable.  Counters accumulate
+/* Pool and scheduler state (the preemption count is section 4.2's
+ * KV-pressure signal); every output is nullable.  Counters accumulate
  * over the engine's life. */
 rp_status rp_kv_status(rp_engine* eng, int64_t* free_pages, int32_t* running,
                        int32_t* waiting, int64_t* preemptions, int64_t* recomputed_tokens);
@@ -379,19 +444,21 @@ typedef struct rp_kernel_stats {
  * Every class starts timing all of its launches (see rp_profile_every). */
 rp_status rp_profile_enable(rp_engine* eng, uint32_t class_mask);
 
-/* Time only one launch in `every` (>= 1) of each selected class: the first,
+/* Time only one launch in `every` (>= 1) of each selected class (the
+ * profiling of section 4.1, sampled): the first,
  * then every `every`-th, counted per class and phase from this call.  The
  * statistics then cover the timed launches only (launches, total_ms, bytes
  * and flops alike), so averages stay unbiased when the sampled launches
  * spread over the workload.  RP_ERR_INVALID_ARG for every < 1. */
 rp_status rp_profile_every(rp_engine* eng, int32_t every);
 
-/* Synchronise, then report and reset the accumulated measurements: one
+/* Synchronise, then report and reset the accumulated measurements of the
+ * section 4.1 profiling: one
  * record per (class, phase) with launches > 0, into host out [cap]. */
 rp_status rp_profile_read(rp_engine* eng, rp_kernel_stats* out, int32_t cap, int32_t* n_out);
 
 /* The practical HBM read ceiling that measurement reports next to the nominal
- * peak (the roofline of the memory-bound decode kernels): streams the
+ * peak (the roofline of the memory-bound decode kernels, section 2.2): streams the
  * caller's device buffer dev_buf (bytes >= 1 MiB, 16-byte aligned; its
  * contents are read, never written) reps times with a read-only kernel in
  * which each of 2048 waves walks its own contiguous share with 8 one-KB
@@ -422,8 +489,8 @@ typedef struct rp_step_record {
  * (0 stops and discards the trace).  Two HIP events bracket each step. */
 rp_status rp_step_trace_enable(rp_engine* eng, int32_t cap);
 
-/* Synchronise, then copy the recorded steps to host out [cap] in order and
- * clear the trace; n_out gets the number copied (steps beyond the enabled
+/* Synchronise, then copy the recorded steps (section 4.1's step-time
+ * profile) to host out [cap] in order and clear the trace; n_out gets the number copied (steps beyond the enabled
  * capacity are not recorded). */
 rp_status rp_step_trace_read(rp_engine* eng, rp_step_record* out, int32_t cap, int32_t* n_out);
 

@@ -10,6 +10,7 @@
 #include "tail_batch.hpp"
 
 #include <algorithm>
+#include <chrono>
 #include <array>
 #include <cmath>
 #include <cstring>
@@ -114,8 +115,9 @@ ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l) {
 }
 
 Engine::Engine(const rp_model_config& cfg, const rp_weights& w, const rp_engine_limits& lim, void* kv_ws,
-               size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, hipStream_t stream)
+               size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, hipStream_t stream, bool no_alloc)
     : cfg_(cfg), lim_(lim), stream_(stream), pool_(lim.kv_pages) {
+  no_alloc_ = no_alloc;
   validate_config(cfg);
   validate_limits(lim);
   bf16_ = cfg.dtype == RP_DTYPE_BF16;
@@ -146,20 +148,20 @@ Engine::Engine(const rp_model_config& cfg, const rp_weights& w, const rp_engine_
   for (int32_t s = lim.max_seqs - 1; s >= 0; --s) free_slots_.push_back(s);
 
   const size_t pt_bytes = static_cast<size_t>(lim.max_seqs) * plan_.max_pages * 4;
-  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_page_table_), pt_bytes, hipHostMallocDefault));
-  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_slot_seed_), lim.max_seqs * 8, hipHostMallocDefault));
-  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_slot_id_), lim.max_seqs * 8, hipHostMallocDefault));
-  HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&h_slot_temp_), lim.max_seqs * 4, hipHostMallocDefault));
+  h_page_table_ = static_cast<int32_t*>(host_buffer(pt_bytes));
+  h_slot_seed_ = static_cast<uint64_t*>(host_buffer(lim.max_seqs * 8));
+  h_slot_id_ = static_cast<uint64_t*>(host_buffer(lim.max_seqs * 8));
+  h_slot_temp_ = static_cast<float*>(host_buffer(lim.max_seqs * 4));
   std::memset(h_page_table_, 0, pt_bytes);
   std::memset(h_slot_seed_, 0, lim.max_seqs * 8);
   std::memset(h_slot_id_, 0, lim.max_seqs * 8);
   std::memset(h_slot_temp_, 0, lim.max_seqs * 4);
-  HIP_TRY(hipEventCreateWithFlags(&ev_tables_, hipEventDisableTiming));
+  if (!no_alloc_) HIP_TRY(hipEventCreateWithFlags(&ev_tables_, hipEventDisableTiming));
   ring_bytes_ = static_cast<size_t>(plan_.meta_ints) * 4;
   ring_.resize(8);
   for (auto& r : ring_) {
-    HIP_TRY(hipHostMalloc(&r.host, ring_bytes_, hipHostMallocDefault));
-    HIP_TRY(hipEventCreateWithFlags(&r.ev, hipEventDisableTiming));
+    r.host = host_buffer(ring_bytes_);
+    if (!no_alloc_) HIP_TRY(hipEventCreateWithFlags(&r.ev, hipEventDisableTiming));
   }
 
   // RoPE table: angle = pos * theta^(-2d/hd), computed in double, stored fp32.
@@ -185,15 +187,17 @@ Engine::Engine(const rp_model_config& cfg, const rp_weights& w, const rp_engine_
 Engine::~Engine() {
   (void)hipStreamSynchronize(stream_);
   for (auto& r : ring_) {
-    if (r.host) (void)hipHostFree(r.host);
+    if (r.host && !no_alloc_) (void)hipHostFree(r.host);
     if (r.ev) (void)hipEventDestroy(r.ev);
   }
   for (auto e : events_) (void)hipEventDestroy(e);
   if (ev_tables_) (void)hipEventDestroy(ev_tables_);
-  if (h_page_table_) (void)hipHostFree(h_page_table_);
-  if (h_slot_seed_) (void)hipHostFree(h_slot_seed_);
-  if (h_slot_id_) (void)hipHostFree(h_slot_id_);
-  if (h_slot_temp_) (void)hipHostFree(h_slot_temp_);
+  if (!no_alloc_) {
+    if (h_page_table_) (void)hipHostFree(h_page_table_);
+    if (h_slot_seed_) (void)hipHostFree(h_slot_seed_);
+    if (h_slot_id_) (void)hipHostFree(h_slot_id_);
+    if (h_slot_temp_) (void)hipHostFree(h_slot_temp_);
+  }
   for (auto& c : eos_free_) {
     (void)hipHostFree(c.host);
     (void)hipEventDestroy(c.ev);
@@ -207,6 +211,44 @@ Engine::~Engine() {
     (void)hipEventDestroy(t.e1);
   }
   for (auto e : trace_pool_) (void)hipEventDestroy(e);
+}
+
+void* Engine::host_buffer(size_t bytes) {
+  if (no_alloc_) {
+    host_store_.emplace_back(std::max<size_t>(bytes, 16));
+    return host_store_.back().data();
+  }
+  void* p = nullptr;
+  HIP_TRY(hipHostMalloc(&p, bytes, hipHostMallocDefault));
+  return p;
+}
+
+void Engine::fence_record(hipEvent_t ev) {
+  if (ev) HIP_TRY(hipEventRecord(ev, stream_));
+}
+
+void Engine::fence_wait(hipEvent_t ev) {
+  if (ev)
+    HIP_TRY(hipEventSynchronize(ev));
+  else
+    HIP_TRY(hipStreamSynchronize(stream_));
+}
+
+void Engine::mark(size_t k) {
+  if (!no_alloc_) {
+    HIP_TRY(hipEventRecord(event_at(k), stream_));
+    return;
+  }
+  HIP_TRY(hipStreamSynchronize(stream_));
+  if (host_marks_.size() <= k) host_marks_.resize(k + 1);
+  host_marks_[k] = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now().time_since_epoch()).count();
+}
+
+double Engine::mark_ms(size_t a, size_t b) {
+  if (no_alloc_) return host_marks_[b] - host_marks_[a];
+  float ms = 0.f;
+  HIP_TRY(hipEventElapsedTime(&ms, events_[a], events_[b]));
+  return ms;
 }
 
 Engine::TraceRec* Engine::trace_begin(int kind, int rows, int64_t sum_ctx) {
@@ -233,6 +275,7 @@ void Engine::trace_end(TraceRec* t) {
 
 void Engine::step_trace_enable(int32_t cap) {
   if (cap < 0) throw RpError(RP_ERR_INVALID_ARG, "trace capacity must be >= 0");
+  if (no_alloc_ && cap > 0) throw RpError(RP_ERR_BAD_STATE, "no step trace without allocations");
   HIP_TRY(hipStreamSynchronize(stream_));
   for (auto& t : trace_) {
     trace_pool_.push_back(t.e0);
@@ -264,6 +307,7 @@ int32_t Engine::step_trace_read(rp_step_record* out, int32_t cap) {
 void Engine::set_eos(int32_t token) {
   if (token < -1 || token >= cfg_.vocab) throw RpError(RP_ERR_INVALID_ARG, "end-of-sequence token out of range");
   if (live_count() != 0) throw RpError(RP_ERR_BAD_STATE, "the end-of-sequence token changes only with no live sequences");
+  if (no_alloc_ && token >= 0) throw RpError(RP_ERR_BAD_STATE, "no end-of-sequence checks without allocations");
   eos_token_ = token;
 }
 
@@ -311,7 +355,7 @@ int32_t* Engine::stage_meta(size_t ints) {
   if (ints * 4 > ring_bytes_) throw RpError(RP_ERR_CAPACITY, "step metadata exceeds the staging capacity");
   Staging& st = ring_[ring_next_];
   if (st.pending) {
-    HIP_TRY(hipEventSynchronize(st.ev));
+    fence_wait(st.ev);
     st.pending = false;
   }
   return static_cast<int32_t*>(st.host);
@@ -320,7 +364,7 @@ int32_t* Engine::stage_meta(size_t ints) {
 void Engine::upload_meta(const int32_t* host, size_t ints) {
   Staging& st = ring_[ring_next_];
   HIP_TRY(hipMemcpyAsync(scratch_ + plan_.meta, host, ints * 4, hipMemcpyHostToDevice, stream_));
-  HIP_TRY(hipEventRecord(st.ev, stream_));
+  fence_record(st.ev);
   st.pending = true;
   ring_next_ = (ring_next_ + 1) % ring_.size();
   d_meta_ = sp<int32_t>(plan_.meta);
@@ -332,7 +376,7 @@ void Engine::upload_slot_tables() {
   HIP_TRY(hipMemcpyAsync(scratch_ + plan_.slot_seed, h_slot_seed_, lim_.max_seqs * 8, hipMemcpyHostToDevice, stream_));
   HIP_TRY(hipMemcpyAsync(scratch_ + plan_.slot_id, h_slot_id_, lim_.max_seqs * 8, hipMemcpyHostToDevice, stream_));
   HIP_TRY(hipMemcpyAsync(scratch_ + plan_.slot_temp, h_slot_temp_, lim_.max_seqs * 4, hipMemcpyHostToDevice, stream_));
-  HIP_TRY(hipEventRecord(ev_tables_, stream_));
+  fence_record(ev_tables_);
   tables_pending_ = true;
 }
 
@@ -633,7 +677,7 @@ std::vector<int32_t> Engine::admit_seqs(const std::vector<AdmitSeq>& a, const st
                                         float* logits_out) {
   const int32_t n = static_cast<int32_t>(a.size());
   if (tables_pending_) {
-    HIP_TRY(hipEventSynchronize(ev_tables_));
+    fence_wait(ev_tables_);
     tables_pending_ = false;
   }
   std::vector<int32_t> new_slots(n);
@@ -833,6 +877,7 @@ void Engine::profile_every(int32_t every) {
 
 void Engine::profile_enable(uint32_t mask) {
   if (mask >> RP_K_COUNT) throw RpError(RP_ERR_INVALID_ARG, "profile mask names an unknown kernel class");
+  if (no_alloc_ && mask) throw RpError(RP_ERR_BAD_STATE, "no profiling without allocations");
   prof_mask_ = mask;
 }
 
@@ -991,7 +1036,7 @@ std::vector<int32_t> Engine::schedule_pages() {
     const int64_t e = extra(s);
     if (e == 0) continue;
     if (!grew && tables_pending_) {
-      HIP_TRY(hipEventSynchronize(ev_tables_));
+      fence_wait(ev_tables_);
       tables_pending_ = false;
     }
     Seq& q = slots_[s];
@@ -1089,11 +1134,10 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
   const int32_t* hist = sp<int32_t>(plan_.hist);
   const float* logp_hist = sp<float>(plan_.logp);
   size_t next = 0;
-  size_t n_ev = 0;
-  hipEvent_t ev_start = event_at(n_ev++);
-  hipEvent_t ev_pre = event_at(n_ev++);
-  hipEvent_t ev_end = event_at(n_ev++);
-  std::vector<std::pair<size_t, int32_t>> left_ev;     // (event index, member position) per departure
+  // time marks: 0 round start, 1 end of the first admission, 2 round end, then one per step with departures
+  const size_t ev_start = 0, ev_pre = 1, ev_end = 2;
+  size_t n_ev = 3;
+  std::vector<std::pair<size_t, int32_t>> left_ev;     // (mark index, member position) per departure
   std::vector<std::array<int64_t, 3>> pending_copies;  // dev offset, host offset, length
   size_t resp_cursor = 0;
   std::unordered_map<int64_t, int32_t> id_member;      // sequence id -> position in members
@@ -1224,29 +1268,27 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     auto goes = [&](int64_t id) { return stop || (race && abort_prompt[race->prompt[id_member.at(id)]]); };
     for (int32_t s : order_)
       if ((slots_[s].finished && settled(slots_[s])) || goes(slots_[s].id)) leaving.push_back(s);
-    bool any = !leaving.empty();
+    std::vector<int64_t> leaving_waiting;
+    if (race)
+      for (const Waiting& w : waiting_)
+        if (id_member.count(w.id) && goes(w.id)) leaving_waiting.push_back(w.id);
+    if (leaving.empty() && leaving_waiting.empty()) return;
+    // Departure time: the end of the step that finished them, before their tokens are copied out.
+    mark(n_ev);
     for (int32_t s : leaving) retire(s);
-    if (race) {
-      for (size_t w = 0; w < waiting_.size();) {
-        if (id_member.count(waiting_[w].id) && goes(waiting_[w].id)) {
-          retire_waiting(waiting_[w]);
-          waiting_.erase(waiting_.begin() + static_cast<std::ptrdiff_t>(w));
-          any = true;
-        } else {
-          ++w;
-        }
-      }
+    for (int64_t id : leaving_waiting) {
+      auto it = std::find_if(waiting_.begin(), waiting_.end(), [&](const Waiting& w) { return w.id == id; });
+      retire_waiting(*it);
+      waiting_.erase(it);
     }
-    if (!any) return;
-    HIP_TRY(hipEventRecord(event_at(n_ev), stream_));
     ++n_ev;
   };
 
-  HIP_TRY(hipEventRecord(ev_start, stream_));
+  mark(ev_start);
   admit();
   if (race && next < members.size())
     throw RpError(RP_ERR_CAPACITY, "a race round must start all of its responses together");
-  HIP_TRY(hipEventRecord(ev_pre, stream_));
+  mark(ev_pre);
   collect();
   while (true) {
     if (next < members.size()) {
@@ -1261,14 +1303,13 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
       drain_eos();  // only finished sequences are left: settle their end-of-sequence checks
     collect();
   }
-  HIP_TRY(hipEventRecord(ev_end, stream_));
+  mark(ev_end);
   flush();
-  HIP_TRY(hipEventSynchronize(ev_end));
+  HIP_TRY(hipStreamSynchronize(stream_));
 
   if (!st) return;
   const int32_t round_id = st->round_id, kind = st->kind;
   *st = rp_round_stats{};
-  float ms = 0.f;
   st->round_id = round_id;
   st->kind = kind;
   st->n_seqs = static_cast<int32_t>(members.size());
@@ -1278,16 +1319,11 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
   st->peak_pages = pool_.peak_used();
   st->preemptions = n_preempt_ - preempt0;
   st->recomputed_tokens = n_recompute_tok_ - recompute0;
-  HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_end));
-  st->makespan_ms = ms;
-  HIP_TRY(hipEventElapsedTime(&ms, ev_start, ev_pre));
-  st->prefill_ms = ms;
+  st->makespan_ms = mark_ms(ev_start, ev_end);
+  st->prefill_ms = mark_ms(ev_start, ev_pre);
   st->decode_ms = st->makespan_ms - st->prefill_ms;
   double idle = 0.0;
-  for (auto& le : left_ev) {
-    HIP_TRY(hipEventElapsedTime(&ms, events_[le.first], ev_end));
-    idle += std::max(0.0, static_cast<double>(ms)) * 1e-3;
-  }
+  for (auto& le : left_ev) idle += std::max(0.0, mark_ms(le.first, ev_end)) * 1e-3;
   st->idle_slot_s = idle;
   const double denom = static_cast<double>(members.size()) * st->makespan_ms * 1e-3;
   st->slot_idle = denom > 0 ? idle / denom : 0.0;

@@ -110,8 +110,13 @@ struct Race {
 
 class Engine {
  public:
+  // no_alloc: the engine then makes no allocating HIP call (no pinned host
+  // memory, no events): staging buffers are ordinary host memory, waits on a
+  // copy or a step become stream synchronisations, and the round statistics
+  // are timed with the host clock after the stream has drained.  End-of-
+  // sequence checks, the step trace and profiling are refused in that mode.
   Engine(const rp_model_config& cfg, const rp_weights& w, const rp_engine_limits& lim, void* kv_ws,
-         size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, hipStream_t stream);
+         size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, hipStream_t stream, bool no_alloc = false);
   ~Engine();
 
   void prefill(int32_t n, const int64_t* ids, const int32_t* toks, const int64_t* offs,
@@ -152,6 +157,17 @@ class Engine {
     hipEvent_t ev = nullptr;
     bool pending = false;
   };
+  // Host buffer of `bytes` for staging copies: pinned normally, ordinary
+  // memory (owned by host_store_) without allocations.
+  void* host_buffer(size_t bytes);
+  // Stream-ordered completion points: a HIP event, or (ev == nullptr, the
+  // no-allocation mode) a stream synchronisation when waited on.
+  void fence_record(hipEvent_t ev);
+  void fence_wait(hipEvent_t ev);
+  // Time marks of run_round: mark k is recorded in stream order; mark_ms(a, b)
+  // is the time between two recorded marks.
+  void mark(size_t k);
+  double mark_ms(size_t a, size_t b);
 
   void forward(int M, bool is_prefill, int n_seq_prefill, int total_items, int total_splits, int tps);
   int32_t* stage_meta(size_t ints);
@@ -246,6 +262,9 @@ class Engine {
   size_t ring_next_ = 0;
   size_t ring_bytes_ = 0;
   bool broken_ = false;
+  bool no_alloc_ = false;
+  std::vector<std::vector<char>> host_store_;  // host buffers of the no-allocation mode
+  std::vector<double> host_marks_;             // mark times (ms, host clock) of the no-allocation mode
   // device metadata views (set by the last stage/upload)
   const int32_t* d_meta_ = nullptr;
   // metadata pointers used by forward()

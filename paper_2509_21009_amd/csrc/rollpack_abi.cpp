@@ -2,8 +2,10 @@
 // Every entry point validates its arguments, converts exceptions into
 // rp_status codes and records a thread-local message for rp_last_error().
 #include <cmath>
+#include <memory>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "engine.hpp"
 #include "tail_batch.hpp"
@@ -49,6 +51,45 @@ rp_status engine_call(rp_engine* eng, F&& f) {
       throw;
     }
   });
+}
+
+// Runs one rollout call of the given schedule mode on a fresh engine (the
+// one-shot entry points).  Returns the number of rounds.
+int32_t run_one_shot(rollpack::Engine& e, int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
+                     const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed, float temperature,
+                     int32_t schedule_mode, const int32_t* round_ids, const rp_tail_params* tail,
+                     int32_t* resp_tokens_out, float* resp_logprobs_out, int32_t* resp_len_out, int32_t* kept_out,
+                     rp_round_stats* stats_out, int32_t max_stats) {
+  using rollpack::RpError;
+  if (max_stats < 0) throw RpError(RP_ERR_INVALID_ARG, "max_stats must be >= 0");
+  if (n < 1) throw RpError(RP_ERR_INVALID_ARG, "n must be >= 1");
+  switch (schedule_mode) {
+    case RP_SCHEDULE_NONE:
+    case RP_SCHEDULE_ROUNDS: {
+      if ((schedule_mode == RP_SCHEDULE_ROUNDS) != (round_ids != nullptr))
+        throw RpError(RP_ERR_INVALID_ARG, "round_ids are given exactly under RP_SCHEDULE_ROUNDS");
+      if (tail) throw RpError(RP_ERR_INVALID_ARG, "tail parameters belong to RP_SCHEDULE_TAIL_BATCHING");
+      const int32_t r = e.rollout(n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
+                                  round_ids, resp_tokens_out, resp_logprobs_out, resp_len_out, stats_out, max_stats);
+      if (kept_out)
+        for (int32_t i = 0; i < n; ++i) kept_out[i] = 1;
+      return r;
+    }
+    case RP_SCHEDULE_TAIL_BATCHING: {
+      if (!tail || round_ids) throw RpError(RP_ERR_INVALID_ARG, "tail batching needs rp_tail_params and no round_ids");
+      if (tail->r_spec < 1 || n % tail->r_spec != 0)
+        throw RpError(RP_ERR_INVALID_ARG, "tail batching: n must be a multiple of r_spec >= 1");
+      const int32_t n_prompts = n / tail->r_spec;
+      std::vector<int32_t> accept(static_cast<size_t>(n_prompts)), kept;
+      if (!kept_out) kept.resize(static_cast<size_t>(n));
+      return e.rollout_tail_batched(n_prompts, tail->r_spec, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens,
+                                    seed, temperature, tail->P0, tail->R0, tail->eta_p, tail->eta_r, resp_tokens_out,
+                                    resp_logprobs_out, resp_len_out, accept.data(), kept_out ? kept_out : kept.data(),
+                                    stats_out, max_stats);
+    }
+    default:
+      throw RpError(RP_ERR_INVALID_ARG, "unknown schedule mode");
+  }
 }
 
 }  // namespace
@@ -141,6 +182,26 @@ rp_status rp_rollout_generate(rp_engine* eng, int32_t n, const int64_t* seq_ids,
     if (max_stats < 0) throw rollpack::RpError(RP_ERR_INVALID_ARG, "max_stats must be >= 0");
     const int32_t r = e->rollout(n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
                                  round_ids, resp_tokens_out, resp_logprobs_out, resp_len_out, stats_out, max_stats);
+    if (n_rounds_out) *n_rounds_out = r;
+  });
+}
+
+rp_status rp_generate(const rp_model_config* cfg, const rp_weights* weights, const rp_engine_limits* limits,
+                      void* kv_ws, size_t kv_bytes, void* scratch_ws, size_t scratch_bytes, void* hip_stream,
+                      int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens, const int64_t* prompt_offsets,
+                      const int32_t* max_new_tokens, uint64_t seed, float temperature, int32_t schedule_mode,
+                      const int32_t* round_ids, const rp_tail_params* tail, int32_t* resp_tokens_out,
+                      float* resp_logprobs_out, int32_t* resp_len_out, int32_t* kept_out, rp_round_stats* stats_out,
+                      int32_t max_stats, int32_t* n_rounds_out) {
+  return guarded([&] {
+    if (!cfg || !weights || !limits) throw rollpack::RpError(RP_ERR_INVALID_ARG, "null argument");
+    rollpack::validate_config(*cfg);
+    rollpack::validate_limits(*limits);
+    std::unique_ptr<rollpack::Engine> e(new rollpack::Engine(*cfg, *weights, *limits, kv_ws, kv_bytes, scratch_ws,
+                                                             scratch_bytes, static_cast<hipStream_t>(hip_stream)));
+    const int32_t r = run_one_shot(*e, n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
+                                   schedule_mode, round_ids, tail, resp_tokens_out, resp_logprobs_out, resp_len_out,
+                                   kept_out, stats_out, max_stats);
     if (n_rounds_out) *n_rounds_out = r;
   });
 }

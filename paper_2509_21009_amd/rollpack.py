@@ -61,6 +61,14 @@ KERNEL_CLASSES = ("embed_norm", "add_norm", "gemm_qkv", "rope_append", "attn", "
                   "gemm_gate_up", "gemm_down", "gemm_lm_head", "sample")
 
 
+class RpTailParams(ctypes.Structure):
+    _fields_ = [("P0", ctypes.c_int32), ("R0", ctypes.c_int32), ("r_spec", ctypes.c_int32),
+                ("eta_p", ctypes.c_float), ("eta_r", ctypes.c_float)]
+
+
+SCHEDULE_NONE, SCHEDULE_ROUNDS, SCHEDULE_TAIL_BATCHING = 0, 1, 2
+
+
 class RpKernelStats(ctypes.Structure):
     _fields_ = [("kernel_class", ctypes.c_int32), ("phase", ctypes.c_int32), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("bytes", ctypes.c_double), ("flops", ctypes.c_double)]
@@ -106,6 +114,11 @@ SIGNATURES = {
     "rp_rollout_generate": (ctypes.c_int, [_P, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P, ctypes.c_uint64,
                                            ctypes.c_float, _I32P, _I32P, _F32P, _I32P, ctypes.POINTER(RpRoundStats),
                                            ctypes.c_int32, _I32P]),
+    "rp_generate": (ctypes.c_int, [ctypes.POINTER(RpModelConfig), ctypes.POINTER(RpWeights),
+                                   ctypes.POINTER(RpEngineLimits), _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P,
+                                   ctypes.c_int32, _I64P, _I32P, _I64P, _I32P, ctypes.c_uint64, ctypes.c_float,
+                                   ctypes.c_int32, _I32P, ctypes.POINTER(RpTailParams), _I32P, _F32P, _I32P, _I32P,
+                                   ctypes.POINTER(RpRoundStats), ctypes.c_int32, _I32P]),
     "rp_rollout_tail_batched": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P,
                                                ctypes.c_uint64, ctypes.c_float, ctypes.c_int32, ctypes.c_int32,
                                                ctypes.c_float, ctypes.c_float, _I32P, _F32P, _I32P, _I32P, _I32P,
@@ -246,6 +259,45 @@ def rp_rollout_generate(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_ne
                                               max_stats, ctypes.byref(nr)))
     st = [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
     return (resp, logp, lens, st) if details else (resp, st)
+
+
+def _generate_args(seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, schedule_mode, round_ids, tail):
+    ids, ids_p = _arr(seq_ids, np.int64)
+    toks, toks_p = _arr(prompt_tokens, np.int32)
+    offs, offs_p = _arr(prompt_offsets, np.int64)
+    mn, mn_p = _arr(max_new_tokens, np.int32)
+    rid, rid_p = _opt(round_ids, np.int32)
+    tp = None if tail is None else ctypes.byref(tail)
+    keep = (ids, toks, offs, mn, rid)
+    return keep, [len(ids), ids_p, toks_p, offs_p, mn_p], rid_p, tp
+
+
+def _generate_outputs(n, total, max_stats):
+    resp = np.zeros(max(total, 1), np.int32)
+    logp = np.zeros(max(total, 1), np.float32)
+    lens = np.zeros(n, np.int32)
+    kept = np.zeros(n, np.int32)
+    stats = (RpRoundStats * max(max_stats, 1))()
+    return resp, logp, lens, kept, stats
+
+
+def rp_generate(cfg: RpModelConfig, weights: RpWeights, limits: RpEngineLimits, kv_ptr: int, kv_bytes: int,
+                scratch_ptr: int, scratch_bytes: int, stream_ptr: int, seq_ids, prompt_tokens, prompt_offsets,
+                max_new_tokens, seed: int, temperature: float, schedule_mode: int = SCHEDULE_NONE, round_ids=None,
+                tail: Optional[RpTailParams] = None, max_stats: int = 64):
+    """One-shot rollout.  Returns (tokens, logprobs, lengths, kept (bool), round stats)."""
+    keep, head, rid_p, tp = _generate_args(seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, schedule_mode,
+                                           round_ids, tail)
+    n, total = head[0], int(keep[3].sum())
+    resp, logp, lens, kept, stats = _generate_outputs(n, total, max_stats)
+    nr = ctypes.c_int32()
+    _check(load_library().rp_generate(ctypes.byref(cfg), ctypes.byref(weights), ctypes.byref(limits), kv_ptr, kv_bytes,
+                                      scratch_ptr, scratch_bytes, stream_ptr, *head, ctypes.c_uint64(seed),
+                                      ctypes.c_float(temperature), schedule_mode, rid_p, tp,
+                                      resp.ctypes.data_as(_I32P), logp.ctypes.data_as(_F32P),
+                                      lens.ctypes.data_as(_I32P), kept.ctypes.data_as(_I32P), stats, max_stats,
+                                      ctypes.byref(nr)))
+    return resp[:total], logp[:total], lens, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
 
 
 def rp_get_logprobs(eng: int, seq_id: int, cap: int) -> np.ndarray:
@@ -417,15 +469,7 @@ class Engine:
         self.kv = torch.empty(kv_bytes, dtype=torch.uint8, device=dev)
         self.scratch = torch.empty(sc_bytes, dtype=torch.uint8, device=dev)
         self.weights = weights
-        self._layers = (RpLayerWeights * shape.layers)()
-        for i, L in enumerate(weights["layers"]):
-            for f in _LAYER_FIELDS:
-                t = L[f]
-                assert t.is_contiguous() and t.device == dev
-                setattr(self._layers[i], f, t.data_ptr())
-        lm = weights.get("lm_head")
-        self._w = RpWeights(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(),
-                            None if lm is None else lm.data_ptr(), self._layers)
+        self._w, self._layers = weights_struct(shape, weights)
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self.handle = rp_engine_create(self.cfg, self._w, self.limits, self.kv.data_ptr(), kv_bytes,
                                        self.scratch.data_ptr(), sc_bytes, self.stream.cuda_stream)
@@ -504,6 +548,38 @@ class Engine:
                              P0: int, R0: int, eta: float, eta_r: Optional[float] = None):
         return rp_rollout_tail_batched(self.handle, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed,
                                        temperature, P0, R0, eta, eta_r)
+
+
+def weights_struct(shape, weights: dict):
+    """(RpWeights, its layer array) pointing at the device tensors of `weights`; keep both alive."""
+    dev = weights["embed"].device
+    layers = (RpLayerWeights * shape.layers)()
+    for i, L in enumerate(weights["layers"]):
+        for f in _LAYER_FIELDS:
+            t = L[f]
+            assert t.is_contiguous() and t.device == dev
+            setattr(layers[i], f, t.data_ptr())
+    lm = weights.get("lm_head")
+    w = RpWeights(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(),
+                  None if lm is None else lm.data_ptr(), layers)
+    return w, layers
+
+
+def generate(shape, weights: dict, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed: int,
+             temperature: float, *, limits: RpEngineLimits, schedule_mode: int = SCHEDULE_NONE, round_ids=None,
+             tail: Optional[RpTailParams] = None, stream=None):
+    """rp_generate with workspaces allocated here from torch (freed when the call returns)."""
+    import torch
+    cfg = model_config(shape)
+    kv_bytes, sc_bytes = rp_workspace_size(cfg, limits)
+    dev = weights["embed"].device
+    kv = torch.empty(kv_bytes, dtype=torch.uint8, device=dev)
+    scratch = torch.empty(sc_bytes, dtype=torch.uint8, device=dev)
+    w, layers = weights_struct(shape, weights)
+    stream = stream if stream is not None else torch.cuda.current_stream(dev)
+    return rp_generate(cfg, w, limits, kv.data_ptr(), kv_bytes, scratch.data_ptr(), sc_bytes, stream.cuda_stream,
+                       seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature, schedule_mode,
+                       round_ids, tail)
 
 
 def weights_for_engine(w: dict) -> dict:

@@ -32,9 +32,37 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for required in ("rp_prefill", "rp_decode_step", "rp_free_finished", "rp_rollout_generate",
-                     "rp_engine_create", "rp_workspace_size", "rp_plan_tail_batching", "rp_last_error"):
+    for required in ("rp_prefill", "rp_decode_step", "rp_free_finished", "rp_rollout_generate", "rp_generate",
+                     "rp_abort", "rp_engine_create", "rp_workspace_size", "rp_plan_tail_batching", "rp_last_error"):
         assert required in names
+
+
+def declaration_comments():
+    """{function name: the comment block right before its declaration}."""
+    text = open(HEADER).read()
+    out = {}
+    for m in re.finditer(r"/\*((?:(?!\*/).)*)\*/\s*(?:typedef[^;]*;\s*)*(?:rp_status|void|const char\*)\s+(rp_[a-z_]+)\s*\(",
+                         text, flags=re.S):
+        out[m.group(2)] = re.sub(r"\s+", " ", re.sub(r"\n\s*\*", " ", m.group(1)))
+    return out
+
+
+def test_core_declarations_cite_the_paper():
+    """Each entry point of the boundary says which passage defines it: section 2.1 (rollout:
+    prefill, decode, generate), section 3 (tail batching), section 5 (add / abort), section 4.x
+    (KV pressure, profiling), or Algorithm 1; the allocation-free variant names its callers."""
+    comments = declaration_comments()
+    infra = {"rp_last_error", "rp_engine_destroy"}
+    missing = [n for n in declared_functions() if n not in infra and n not in comments]
+    assert not missing, missing
+    uncited = [n for n, c in comments.items() if n not in infra and
+               not re.search(r"section \d|Algorithm 1|cannot allocate", c)]
+    assert not uncited, uncited
+    for name, cites in {"rp_prefill": "section 2.1", "rp_decode_step": "section 2.1", "rp_generate": "section 2.1",
+                        "rp_rollout_generate": "section 2.1", "rp_abort": "section 5",
+                        "rp_rollout_tail_batched": "section 3", "rp_plan_tail_batching": "section 3",
+                        "rp_free_finished": "Algorithm 1"}.items():
+        assert cites in comments[name], (name, cites)
 
 
 def test_library_exports_every_declared_symbol(lib):
