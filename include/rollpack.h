@@ -306,6 +306,34 @@ rp_status rp_generate(const rp_model_config* cfg, const rp_weights* weights, con
                       int32_t* resp_len_out, int32_t* kept_out, rp_round_stats* stats_out, int32_t max_stats,
                       int32_t* n_rounds_out);
 
+/* rp_generate for callers that cannot allocate: code that runs where
+ * hipMalloc, pinned host allocations or event creation are not allowed, tight
+ * serving loops, harnesses that forbid allocation.  The arguments and outputs
+ * are rp_generate's without the two workspaces: the KV pool and the scratch
+ * workspace come from one device array that the library holds, 64 MiB
+ * (67,108,864 bytes) per GPU until the process ends, on the current device
+ * (hip_stream, when not NULL, must belong to it).  The call makes no
+ * allocating HIP call: staging goes through ordinary host memory and waits
+ * are stream synchronisations, so it is slower per step than rp_generate,
+ * and the round times in stats_out come from the host clock.
+ *   Limits: kv_bytes + scratch_bytes of rp_workspace_size for these limits
+ *   must not exceed the array (RP_ERR_CAPACITY otherwise, with the sizes in
+ *   the message); about the tiny model or a few 0.5B-shape sequences of a
+ *   few hundred tokens.
+ *   Sharing: every call on a GPU uses that GPU's one array, which keeps the
+ *   last call's contents; the engine clears what must start at zero (the KV
+ *   pool, the page table, the current tokens).  Calls in one process are
+ *   serialised by a lock; overlapping calls on one GPU from code that
+ *   bypassed it would race on the array. */
+rp_status rp_generate_static(const rp_model_config* cfg, const rp_weights* weights,
+                             const rp_engine_limits* limits, void* hip_stream, int32_t n,
+                             const int64_t* seq_ids, const int32_t* prompt_tokens,
+                             const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed,
+                             float temperature, int32_t schedule_mode, const int32_t* round_ids,
+                             const rp_tail_params* tail, int32_t* resp_tokens_out,
+                             float* resp_logprobs_out, int32_t* resp_len_out, int32_t* kept_out,
+                             rp_round_stats* stats_out, int32_t max_stats, int32_t* n_rounds_out);
+
 /* Tail batching run online on the engine (section 3).  n_prompts prompts,
  * submitted in order, each with r_spec = ceil(eta_r * R0) candidate responses;
  * response r of prompt p is sequence seq_ids[p * r_spec + r] with forced

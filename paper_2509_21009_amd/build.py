@@ -27,7 +27,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-munsafe-fp-atomics"]
 
-SOURCES = ["k_gemm.hip", "k_attention.hip", "k_elementwise.hip", "engine.cpp", "tail_batch.cpp",
+SOURCES = ["k_gemm.hip", "k_attention.hip", "k_elementwise.hip", "static_ws.hip", "engine.cpp", "tail_batch.cpp",
            "rollpack_abi.cpp"]
 
 

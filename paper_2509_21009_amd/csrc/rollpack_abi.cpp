@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "engine.hpp"
+#include "static_ws.hpp"
 #include "tail_batch.hpp"
 
 namespace {
@@ -200,6 +201,47 @@ rp_status rp_generate(const rp_model_config* cfg, const rp_weights* weights, con
     std::unique_ptr<rollpack::Engine> e(new rollpack::Engine(*cfg, *weights, *limits, kv_ws, kv_bytes, scratch_ws,
                                                              scratch_bytes, static_cast<hipStream_t>(hip_stream)));
     const int32_t r = run_one_shot(*e, n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
+                                   schedule_mode, round_ids, tail, resp_tokens_out, resp_logprobs_out, resp_len_out,
+                                   kept_out, stats_out, max_stats);
+    if (n_rounds_out) *n_rounds_out = r;
+  });
+}
+
+rp_status rp_generate_static(const rp_model_config* cfg, const rp_weights* weights, const rp_engine_limits* limits,
+                             void* hip_stream, int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
+                             const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed,
+                             float temperature, int32_t schedule_mode, const int32_t* round_ids,
+                             const rp_tail_params* tail, int32_t* resp_tokens_out, float* resp_logprobs_out,
+                             int32_t* resp_len_out, int32_t* kept_out, rp_round_stats* stats_out, int32_t max_stats,
+                             int32_t* n_rounds_out) {
+  return guarded([&] {
+    using rollpack::RpError;
+    if (!cfg || !weights || !limits) throw RpError(RP_ERR_INVALID_ARG, "null argument");
+    rollpack::validate_config(*cfg);
+    rollpack::validate_limits(*limits);
+    const size_t kv = rollpack::kv_pool_bytes(*cfg, limits->kv_pages);  // a multiple of 256
+    const size_t sc = rollpack::plan_scratch(*cfg, *limits).total;
+    if (kv + sc > rollpack::kStaticWorkspaceBytes)
+      throw RpError(RP_ERR_CAPACITY, "rp_generate_static: these limits need " + std::to_string(kv + sc) +
+                                         " bytes of KV pool and scratch; the library's static workspace holds " +
+                                         std::to_string(rollpack::kStaticWorkspaceBytes));
+    auto check = [](hipError_t e, const char* what) {
+      if (e != hipSuccess) throw RpError(RP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+    };
+    int dev = -1;
+    check(hipGetDevice(&dev), "hipGetDevice");
+    const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    if (stream) {
+      hipDevice_t sdev = -1;
+      check(hipStreamGetDevice(stream, &sdev), "hipStreamGetDevice");
+      if (sdev != dev) throw RpError(RP_ERR_INVALID_ARG, "rp_generate_static: the stream belongs to another device");
+    }
+    std::lock_guard<std::mutex> hold(rollpack::static_workspace_lock());
+    void* base = nullptr;
+    check(rollpack::static_workspace(dev, &base), "hipGetSymbolAddress");
+    char* b = static_cast<char*>(base);
+    rollpack::Engine e(*cfg, *weights, *limits, b, kv, b + kv, sc, stream, /*no_alloc=*/true);
+    const int32_t r = run_one_shot(e, n, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed, temperature,
                                    schedule_mode, round_ids, tail, resp_tokens_out, resp_logprobs_out, resp_len_out,
                                    kept_out, stats_out, max_stats);
     if (n_rounds_out) *n_rounds_out = r;

@@ -119,6 +119,11 @@ SIGNATURES = {
                                    ctypes.c_int32, _I64P, _I32P, _I64P, _I32P, ctypes.c_uint64, ctypes.c_float,
                                    ctypes.c_int32, _I32P, ctypes.POINTER(RpTailParams), _I32P, _F32P, _I32P, _I32P,
                                    ctypes.POINTER(RpRoundStats), ctypes.c_int32, _I32P]),
+    "rp_generate_static": (ctypes.c_int, [ctypes.POINTER(RpModelConfig), ctypes.POINTER(RpWeights),
+                                          ctypes.POINTER(RpEngineLimits), _P, ctypes.c_int32, _I64P, _I32P, _I64P,
+                                          _I32P, ctypes.c_uint64, ctypes.c_float, ctypes.c_int32, _I32P,
+                                          ctypes.POINTER(RpTailParams), _I32P, _F32P, _I32P, _I32P,
+                                          ctypes.POINTER(RpRoundStats), ctypes.c_int32, _I32P]),
     "rp_rollout_tail_batched": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P,
                                                ctypes.c_uint64, ctypes.c_float, ctypes.c_int32, ctypes.c_int32,
                                                ctypes.c_float, ctypes.c_float, _I32P, _F32P, _I32P, _I32P, _I32P,
@@ -297,6 +302,24 @@ def rp_generate(cfg: RpModelConfig, weights: RpWeights, limits: RpEngineLimits, 
                                       resp.ctypes.data_as(_I32P), logp.ctypes.data_as(_F32P),
                                       lens.ctypes.data_as(_I32P), kept.ctypes.data_as(_I32P), stats, max_stats,
                                       ctypes.byref(nr)))
+    return resp[:total], logp[:total], lens, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
+
+
+def rp_generate_static(cfg: RpModelConfig, weights: RpWeights, limits: RpEngineLimits, stream_ptr: int, seq_ids,
+                       prompt_tokens, prompt_offsets, max_new_tokens, seed: int, temperature: float,
+                       schedule_mode: int = SCHEDULE_NONE, round_ids=None, tail: Optional[RpTailParams] = None,
+                       max_stats: int = 64):
+    """rp_generate over the library's static workspace.  Returns what rp_generate returns."""
+    keep, head, rid_p, tp = _generate_args(seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, schedule_mode,
+                                           round_ids, tail)
+    n, total = head[0], int(keep[3].sum())
+    resp, logp, lens, kept, stats = _generate_outputs(n, total, max_stats)
+    nr = ctypes.c_int32()
+    _check(load_library().rp_generate_static(ctypes.byref(cfg), ctypes.byref(weights), ctypes.byref(limits),
+                                             stream_ptr, *head, ctypes.c_uint64(seed), ctypes.c_float(temperature),
+                                             schedule_mode, rid_p, tp, resp.ctypes.data_as(_I32P),
+                                             logp.ctypes.data_as(_F32P), lens.ctypes.data_as(_I32P),
+                                             kept.ctypes.data_as(_I32P), stats, max_stats, ctypes.byref(nr)))
     return resp[:total], logp[:total], lens, kept.astype(bool), [stats[i].as_dict() for i in range(min(nr.value, max_stats))]
 
 
