@@ -510,6 +510,9 @@ typedef struct rp_step_record {
   int32_t reserved;
   int64_t sum_ctx;
   double ms;
+  double end_ms;     /* from the start of its round (the round's makespan origin) to the end of
+                        this step; -1 outside a rollout call.  A sequence's finish time in the
+                        round statistics is end_ms of the step that produced its last token. */
 } rp_step_record;
 
 /* Per-step trace, the measurement behind the paper's step-time profiles

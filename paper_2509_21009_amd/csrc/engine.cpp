@@ -210,6 +210,7 @@ Engine::~Engine() {
     (void)hipEventDestroy(t.e0);
     (void)hipEventDestroy(t.e1);
   }
+  for (auto e : trace_round_evs_) (void)hipEventDestroy(e);
   for (auto e : trace_pool_) (void)hipEventDestroy(e);
 }
 
@@ -251,19 +252,21 @@ double Engine::mark_ms(size_t a, size_t b) {
   return ms;
 }
 
+hipEvent_t Engine::trace_event() {
+  hipEvent_t e;
+  if (!trace_pool_.empty()) {
+    e = trace_pool_.back();
+    trace_pool_.pop_back();
+  } else {
+    HIP_TRY(hipEventCreate(&e));
+  }
+  return e;
+}
+
 Engine::TraceRec* Engine::trace_begin(int kind, int rows, int64_t sum_ctx) {
   if (static_cast<int32_t>(trace_.size()) >= trace_cap_) return nullptr;
-  auto take = [&]() {
-    hipEvent_t e;
-    if (!trace_pool_.empty()) {
-      e = trace_pool_.back();
-      trace_pool_.pop_back();
-    } else {
-      HIP_TRY(hipEventCreate(&e));
-    }
-    return e;
-  };
-  TraceRec t{rp_step_record{kind, cur_round_, rows, 0, sum_ctx, 0.0}, take(), take()};
+  TraceRec t{rp_step_record{kind, cur_round_, rows, 0, sum_ctx, 0.0, -1.0}, trace_event(), trace_event(),
+             cur_round_ev_};
   HIP_TRY(hipEventRecord(t.e0, stream_));
   trace_.push_back(t);
   return &trace_.back();
@@ -282,6 +285,8 @@ void Engine::step_trace_enable(int32_t cap) {
     trace_pool_.push_back(t.e1);
   }
   trace_.clear();
+  for (auto e : trace_round_evs_) trace_pool_.push_back(e);
+  trace_round_evs_.clear();
   trace_.reserve(static_cast<size_t>(cap));  // pointers handed out by trace_begin stay valid
   trace_cap_ = cap;
 }
@@ -295,12 +300,21 @@ int32_t Engine::step_trace_read(rp_step_record* out, int32_t cap) {
     HIP_TRY(hipEventElapsedTime(&ms, trace_[i].e0, trace_[i].e1));
     out[i] = trace_[i].rec;
     out[i].ms = ms;
+    if (trace_[i].round_start) {
+      HIP_TRY(hipEventElapsedTime(&ms, trace_[i].round_start, trace_[i].e1));
+      out[i].end_ms = ms;
+    }
   }
   for (auto& t : trace_) {
     trace_pool_.push_back(t.e0);
     trace_pool_.push_back(t.e1);
   }
   trace_.clear();
+  // a running round keeps its start event for the steps still to come
+  for (auto e : trace_round_evs_)
+    if (e != cur_round_ev_) trace_pool_.push_back(e);
+  trace_round_evs_.clear();
+  if (cur_round_ev_) trace_round_evs_.push_back(cur_round_ev_);
   return n;
 }
 
@@ -1285,6 +1299,11 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
   };
 
   mark(ev_start);
+  if (trace_cap_ > 0) {  // the trace's own copy of the round start, kept until the trace is read
+    cur_round_ev_ = trace_event();
+    HIP_TRY(hipEventRecord(cur_round_ev_, stream_));
+    trace_round_evs_.push_back(cur_round_ev_);
+  }
   admit();
   if (race && next < members.size())
     throw RpError(RP_ERR_CAPACITY, "a race round must start all of its responses together");
@@ -1304,6 +1323,7 @@ void Engine::run_round(const std::vector<int32_t>& members, const SeqArrays& a, 
     collect();
   }
   mark(ev_end);
+  cur_round_ev_ = nullptr;
   flush();
   HIP_TRY(hipStreamSynchronize(stream_));
 

@@ -238,7 +238,11 @@ class Engine {
   struct TraceRec {
     rp_step_record rec;
     hipEvent_t e0, e1;
+    hipEvent_t round_start;  // recorded at its round's start (nullptr outside a rollout call)
   };
+  hipEvent_t trace_event();
+  hipEvent_t cur_round_ev_ = nullptr;          // round-start event of the running round (trace on)
+  std::vector<hipEvent_t> trace_round_evs_;    // round-start events referenced by trace_
   std::vector<TraceRec> trace_;
   std::vector<hipEvent_t> trace_pool_;
   int32_t trace_cap_ = 0;

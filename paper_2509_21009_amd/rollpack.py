@@ -80,7 +80,8 @@ class RpKernelStats(ctypes.Structure):
 
 class RpStepRecord(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("round_id", ctypes.c_int32), ("rows", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("sum_ctx", ctypes.c_int64), ("ms", ctypes.c_double)]
+                ("reserved", ctypes.c_int32), ("sum_ctx", ctypes.c_int64), ("ms", ctypes.c_double),
+                ("end_ms", ctypes.c_double)]
 
 
 class RollpackError(RuntimeError):
@@ -416,15 +417,15 @@ def rp_step_trace_enable(eng: int, cap: int) -> None:
 
 
 def rp_step_trace_read(eng: int, cap: int) -> np.ndarray:
-    """Structured array of the recorded steps: kind, round_id, rows, sum_ctx, ms."""
+    """Structured array of the recorded steps: kind, round_id, rows, sum_ctx, ms, end_ms."""
     out = (RpStepRecord * max(cap, 1))()
     n = ctypes.c_int32()
     _check(load_library().rp_step_trace_read(eng, out, cap, ctypes.byref(n)))
     rec = np.zeros(n.value, dtype=[("kind", np.int32), ("round_id", np.int32), ("rows", np.int32),
-                                   ("sum_ctx", np.int64), ("ms", np.float64)])
+                                   ("sum_ctx", np.int64), ("ms", np.float64), ("end_ms", np.float64)])
     for i in range(n.value):
         r = out[i]
-        rec[i] = (r.kind, r.round_id, r.rows, r.sum_ctx, r.ms)
+        rec[i] = (r.kind, r.round_id, r.rows, r.sum_ctx, r.ms, r.end_ms)
     return rec
 
 

@@ -42,9 +42,28 @@ class ParityResult:
     worst: tuple
 
 
+ORACLE_CHUNK = 2048
+
+
 def oracle_rollout(w64, shape, prompt, n_new, temperature, seed, seq_id, rnd=None):
+    """oracle.model.generate with the seeded sampler, the prompt prefilled in pieces of
+    ORACLE_CHUNK tokens (KVState.step is incremental: pieces equal one whole step up to the
+    order of fp64 sums, and bound the [queries, keys] score matrices of long prompts)."""
     sample_fn = osm.sampler(temperature, seed, seq_id)
-    return om.generate(w64, shape, prompt, n_new, sample_fn, rnd)
+    if len(prompt) <= ORACLE_CHUNK:
+        return om.generate(w64, shape, prompt, n_new, sample_fn, rnd)
+    st = om.KVState(shape, rnd)
+    for o in range(0, len(prompt), ORACLE_CHUNK):
+        logits = st.step(w64, prompt[o:o + ORACLE_CHUNK])[-1]
+    p = len(prompt)
+    toks, rows = [], []
+    for j in range(n_new):
+        t = int(sample_fn(logits, p + j))
+        toks.append(t)
+        rows.append(logits)
+        if j + 1 < n_new:
+            logits = st.step(w64, [t])[-1]
+    return np.array(toks, np.int32), np.array(rows)
 
 
 def teacher_forced_parity(eng, shape, w64, wl, n_new, tol, temperature, seed, rnd=None, check=None):

@@ -175,3 +175,39 @@ def test_bf16_prompt_cut_into_prefill_pieces():
     eng.close()
     log(f"prefill pieces: {r}")
     assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, r
+
+
+def test_pressured_rollout_matches_the_oracle(tiny):
+    """Preemption by recompute against the oracle itself (not only against an unpressured
+    GPU run): with a pool of 12 pages for 12 sequences that need 24, every sequence's seeded
+    T = 1 tokens equal oracle.model.generate with the oracle's sampler up to the first
+    position whose top-2 score margin is within 1e-4 of the logits' scale (after a near-tie
+    the two fp32/fp64 paths may legitimately diverge)."""
+    from oracle import model as om
+    from oracle import sampling as osm
+    from workloads import weights_to_numpy
+    s, wd = tiny
+    R = rp()
+    w64 = weights_to_numpy({k: v for k, v in wd.items()})
+    ids, toks, offs, mn = _batch(s, 12, 3)
+    eng = _engine(s, wd, 16, 48, 128, 12)
+    eng.set_kv_policy(R.KV_ON_DEMAND)
+    got, st = eng.rollout(ids, toks, offs, mn, 9, 1.0)
+    eng.close()
+    log(f"pressured vs oracle: {st[0]['preemptions']} preemptions, {st[0]['recomputed_tokens']} tokens recomputed")
+    assert st[0]["preemptions"] > 0
+    resp_off = np.concatenate([[0], np.cumsum(mn)])
+    full = 0
+    for i in range(12):
+        ref, logits = om.generate(w64, s, toks[offs[i]:offs[i + 1]], int(mn[i]), osm.sampler(1.0, 9, int(ids[i])))
+        mine = got[resp_off[i]:resp_off[i + 1]]
+        p = int(offs[i + 1] - offs[i])
+        for j in range(int(mn[i])):
+            sc = osm.scores(logits[j], 1.0, 9, int(ids[i]), p + j)
+            if osm.top2_gap(sc) <= 1e-4 * np.max(np.abs(logits[j])):
+                break
+            assert mine[j] == ref[j], (i, j)
+        else:
+            full += 1
+    log(f"pressured vs oracle: {full}/12 sequences identical over all their tokens")
+    assert full >= 10
