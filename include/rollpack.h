@@ -154,6 +154,27 @@ rp_status rp_engine_create(const rp_model_config* cfg, const rp_weights* weights
 
 void rp_engine_destroy(rp_engine* eng);
 
+/* Bytes of the packed copy of a bf16 model's decode weights (every q/k/v, o,
+ * gate, up and down projection and the LM head, each 256-byte aligned), the
+ * stream every memory-bound decode step reads (section 2.2); 0 for an fp32
+ * model. */
+rp_status rp_packed_weights_bytes(const rp_model_config* cfg, size_t* bytes);
+
+/* Give the engine a caller-owned device workspace of at least
+ * rp_packed_weights_bytes bytes (256-byte aligned) for a packed copy of its
+ * weights.  Decoding is memory-bound (section 2.2): each decode step streams
+ * every weight once, and the copy lays each 16-row by 64-column block of a
+ * weight matrix out as the two contiguous 1 KB runs that one wave's loads
+ * read, so the decode GEMMs (16-64 live rows) stream it with non-temporal
+ * 1 KB loads; the products are bit-identical to those of the row-major
+ * weights.  The packing runs on the engine's stream (one read of the
+ * weights); the workspace must stay valid until the engine is destroyed or
+ * this call is made again.  packed_ws NULL goes back to the row-major
+ * weights.  Prefill and batches above 64 rows keep reading the caller's
+ * row-major weights.  Errors: RP_ERR_INVALID_ARG for an fp32 model, a small
+ * or misaligned workspace. */
+rp_status rp_engine_set_packed_weights(rp_engine* eng, void* packed_ws, size_t bytes);
+
 /* Admit n sequences and run their prompts through the model (prefill), then
  * sample each sequence's first response token.  Paper: the actor is given
  * prompts and generates responses for them (section 2.1); admitting a request

@@ -34,11 +34,12 @@ def _between(text: str, start: str, end: str) -> str:
 
 
 def deep_source_digest(root: str = ROOT) -> str:
-    """SHA-256 over what the counters measured: the k_gemm_deep kernel, its launch plan (the
-    instantiated configurations and plan_deep) and the device helpers it uses.  Edits elsewhere in
+    """SHA-256 over what the counters measured: the k_gemm_deep kernel and its weight-load helper,
+    its launch plan (the instantiated configurations and plan_deep) and the device helpers it uses.  Edits elsewhere in
     the GEMM source leave it unchanged."""
     gemm = open(os.path.join(root, SOURCE)).read()
-    parts = [_between(gemm, "template <int R, int MT, int D, bool SILU>\n__global__ __launch_bounds__(256) "
+    parts = [_between(gemm, "template <bool PACKED>\n__device__ __forceinline__ bf16x8_t load_w16", "\n}\n"),
+             _between(gemm, "template <int R, int MT, int D, bool SILU, bool PACKED>\n__global__ __launch_bounds__(256) "
                             "void k_gemm_deep", "\n}\n"),
              _between(gemm, "constexpr DeepCfg kDeepCfg", "\n};\n"),
              _between(gemm, "GemmPlan plan_deep(", "\n}\n"),
@@ -50,7 +51,7 @@ SHAPE = {"H": 3584, "I": 18944}  # Qwen2.5-7B hidden and intermediate sizes
 
 def gate_up_tiles(name: str):
     """Activation tiles of a gate/up (SiLU) deep-GEMM instantiation, else None."""
-    m = re.search(r"k_gemm_deep<(\d+), (\d+), (\d+), true>", name)
+    m = re.search(r"k_gemm_deep<(\d+), (\d+), (\d+), true(?:, (?:true|false))?>", name)
     return int(m.group(2)) if m else None
 
 

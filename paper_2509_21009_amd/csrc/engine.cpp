@@ -62,6 +62,14 @@ void validate_limits(const rp_engine_limits& l) {
                   "2 <= max_context <= 65536");
 }
 
+size_t packed_weights_bytes(const rp_model_config& c) {
+  if (c.dtype != RP_DTYPE_BF16) return 0;
+  const size_t H = c.hidden, I = c.intermediate, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
+  const size_t layer = align256(nq * hd * H * 2) + 2 * align256(nkv * hd * H * 2) + align256(H * nq * hd * 2) +
+                       2 * align256(I * H * 2) + align256(H * I * 2);
+  return layer * c.n_layers + align256(static_cast<size_t>(c.vocab) * H * 2);
+}
+
 size_t kv_pool_bytes(const rp_model_config& c, int64_t pages) {
   const size_t esz = c.dtype == RP_DTYPE_BF16 ? 2 : 4;
   return align256(static_cast<size_t>(pages) * c.n_layers * 2 * c.n_kv_heads * kPageTokens * c.head_dim * esz);
@@ -534,9 +542,11 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     char* kpool = kv_ + static_cast<size_t>(l) * layer_kv_bytes_;
     char* vpool = kv_ + static_cast<size_t>(cfg_.n_layers + l) * layer_kv_bytes_;
 
+    const rp_layer_weights* P = packed_layers_.empty() ? nullptr : &packed_layers_[l];
     GemmArgs g{};
     g.A = h; g.lda = H; g.M = M; g.N = nqkv_; g.K = H;
     g.W = WSeg{{L.wq, L.wk, L.wv}, {nq * hd, nkv * hd, nkv * hd}, 3};
+    if (P) g.Wp = WSeg{{P->wq, P->wk, P->wv}, {nq * hd, nkv * hd, nkv * hd}, 3};
     g.epi = kEpiPartial; g.splits = s_qkv; g.part = part;
     launch_timed(RP_K_GEMM_QKV, gemm_bytes(Md, nqkv_, H, 4), 2.0 * Md * nqkv_ * H,
                  [&] { return launch_gemm(bf16_, g, s); });
@@ -569,6 +579,7 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     g = GemmArgs{};
     g.A = attn; g.lda = nq * hd; g.M = M; g.N = H; g.K = nq * hd;
     g.W = WSeg{{L.wo, nullptr, nullptr}, {H, 0, 0}, 1};
+    if (P) g.Wp = WSeg{{P->wo, nullptr, nullptr}, {H, 0, 0}, 1};
     g.epi = kEpiPartial; g.splits = s_o; g.part = part;
     launch_timed(RP_K_GEMM_O, gemm_bytes(Md, H, nq * hd, 4), 2.0 * Md * H * nq * hd,
                  [&] { return launch_gemm(bf16_, g, s); });
@@ -579,6 +590,7 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     g = GemmArgs{};
     g.A = h; g.lda = H; g.M = M; g.N = I; g.K = H;
     g.W = WSeg{{L.w_gate, L.w_up, nullptr}, {I, I, 0}, 2};
+    if (P) g.Wp = WSeg{{P->w_gate, P->w_up, nullptr}, {I, I, 0}, 2};
     g.epi = kEpiSiluMul; g.splits = 1; g.act_out = act;
     launch_timed(RP_K_GEMM_GATE_UP, gemm_bytes(Md, 2.0 * I, H, 0) + Md * I * e, 4.0 * Md * I * H,
                  [&] { return launch_gemm(bf16_, g, s); });
@@ -586,6 +598,7 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
     g = GemmArgs{};
     g.A = act; g.lda = I; g.M = M; g.N = H; g.K = I;
     g.W = WSeg{{L.w_down, nullptr, nullptr}, {H, 0, 0}, 1};
+    if (P) g.Wp = WSeg{{P->w_down, nullptr, nullptr}, {H, 0, 0}, 1};
     g.epi = kEpiPartial; g.splits = s_d; g.part = part;
     launch_timed(RP_K_GEMM_DOWN, gemm_bytes(Md, H, I, 4), 2.0 * Md * H * I, [&] { return launch_gemm(bf16_, g, s); });
 
@@ -604,6 +617,7 @@ void Engine::forward(int M, bool pre, int n_seq, int total_items, int total_spli
   GemmArgs g{};
   g.A = lm_in; g.lda = H; g.M = m_lm; g.N = V; g.K = H;
   g.W = WSeg{{w_.lm_head, nullptr, nullptr}, {V, 0, 0}, 1};
+  if (packed_lm_) g.Wp = WSeg{{packed_lm_, nullptr, nullptr}, {V, 0, 0}, 1};
   g.epi = kEpiPartial; g.splits = 1; g.part = sp<float>(plan_.logits);
   launch_timed(RP_K_GEMM_LM_HEAD, gemm_bytes(m_lm, V, H, 4), 2.0 * m_lm * V * H,
                [&] { return launch_gemm(bf16_, g, s); });
@@ -881,6 +895,41 @@ int32_t Engine::decode_step(const int32_t* forced, float* logits_out, int64_t* r
     if (q.n_gen >= q.max_new) q.finished = true;
   }
   return B;
+}
+
+void Engine::set_packed_weights(void* ws, size_t bytes) {
+  if (!ws) {
+    HIP_TRY(hipStreamSynchronize(stream_));  // launches already queued may still read the packed copy
+    packed_layers_.clear();
+    packed_lm_ = nullptr;
+    return;
+  }
+  if (!bf16_) throw RpError(RP_ERR_INVALID_ARG, "packed weights apply to bf16 models only");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) throw RpError(RP_ERR_INVALID_ARG, "packed workspace must be 256-byte aligned");
+  if (bytes < packed_weights_bytes(cfg_)) throw RpError(RP_ERR_INVALID_ARG, "packed workspace smaller than rp_packed_weights_bytes");
+  const int H = cfg_.hidden, I = cfg_.intermediate, qd = cfg_.n_q_heads * cfg_.head_dim,
+            kvd = cfg_.n_kv_heads * cfg_.head_dim;
+  char* p = static_cast<char*>(ws);
+  auto pack = [&](const void* w, int rows, int K) {
+    void* dst = p;
+    HIP_TRY(launch_pack_weights(w, dst, rows, K, stream_));
+    p += align256(static_cast<size_t>(rows) * K * 2);
+    return static_cast<const void*>(dst);
+  };
+  std::vector<rp_layer_weights> pl(layers_.size());
+  for (size_t l = 0; l < layers_.size(); ++l) {
+    const rp_layer_weights& L = layers_[l];
+    pl[l] = L;  // norms and biases stay the caller's
+    pl[l].wq = pack(L.wq, qd, H);
+    pl[l].wk = pack(L.wk, kvd, H);
+    pl[l].wv = pack(L.wv, kvd, H);
+    pl[l].wo = pack(L.wo, H, qd);
+    pl[l].w_gate = pack(L.w_gate, I, H);
+    pl[l].w_up = pack(L.w_up, I, H);
+    pl[l].w_down = pack(L.w_down, H, I);
+  }
+  packed_lm_ = pack(w_.lm_head, cfg_.vocab, H);
+  packed_layers_ = std::move(pl);
 }
 
 void Engine::profile_every(int32_t every) {

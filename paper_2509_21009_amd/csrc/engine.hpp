@@ -35,6 +35,9 @@ struct ScratchPlan {
 };
 
 ScratchPlan plan_scratch(const rp_model_config& c, const rp_engine_limits& l);
+// Bytes of the packed copy of the decode-GEMM weights (every projection and
+// the LM head), each tensor 256-byte aligned; 0 for the fp32 model.
+size_t packed_weights_bytes(const rp_model_config& c);
 size_t kv_pool_bytes(const rp_model_config& c, int64_t pages);
 void validate_config(const rp_model_config& c);
 void validate_limits(const rp_engine_limits& l);
@@ -138,6 +141,10 @@ class Engine {
                                int32_t* accept_round_out, int32_t* kept_out, rp_round_stats* stats,
                                int32_t max_stats);
 
+  // Packs every projection and the LM head into the caller's workspace (on the
+  // engine's stream) and points the decode GEMMs at the packed copy from then
+  // on; nullptr goes back to the row-major weights.
+  void set_packed_weights(void* ws, size_t bytes);
   void profile_enable(uint32_t mask);
   void profile_every(int32_t every);
   int32_t profile_read(rp_kernel_stats* out, int32_t cap);
@@ -212,6 +219,8 @@ class Engine {
   rp_engine_limits lim_;
   std::vector<rp_layer_weights> layers_;
   rp_weights w_;
+  std::vector<rp_layer_weights> packed_layers_;  // empty: no packed copy
+  const void* packed_lm_ = nullptr;
   hipStream_t stream_;
   bool bf16_;
   size_t esz_;

@@ -10,7 +10,9 @@
 //    from HBM through buffer loads into a ring of register stages; a stage
 //    is a 64-wide K unit in which each lane reads 32 contiguous bytes of a
 //    row, so one wave's two back-to-back loads cover the row's whole
-//    128-byte line.  Activations (L2-resident) are loaded one stage ahead
+//    128-byte line.  With the packed copy of the weights (launch_pack_weights)
+//    each load instruction reads one contiguous 1 KB run instead, non-temporal
+//    (the weights are read once per step), the same operands in every lane.  Activations (L2-resident) are loaded one stage ahead
 //    into a single buffer.  The block's 4 waves take interleaved K units and
 //    reduce through LDS; blockIdx.y splits K further (fp32 partials).
 //  * k_gemm_stream (M <= 64, the remaining decode shapes): the weights are streamed
@@ -289,7 +291,14 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a, int chunks_per_
 // block's K range, so the block reads whole 512-byte runs of each row.
 // Weight fragments use one buffer resource each: rows past the end of the
 // matrix (the ragged last block) read as zeros and are never stored.
-template <int R, int MT, int D, bool SILU>
+// Weight loads of the deep kernel: row-major (plain) or packed (non-temporal:
+// aux bit 1 is the nt cache policy).
+template <bool PACKED>
+__device__ __forceinline__ bf16x8_t load_w16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, PACKED ? 2 : 0));
+}
+
+template <int R, int MT, int D, bool SILU, bool PACKED>
 __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_split) {
   static_assert(!SILU || R % 2 == 0, "SiLU pairs gate and up fragments");
   constexpr int NACC = R * MT;
@@ -304,6 +313,7 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
   const int nk = nblk > wave ? (nblk - wave + 3) / 4 : 0;
   const uint32_t row_bytes = static_cast<uint32_t>(K) * 2u;
 
+  const WSeg& W = PACKED ? a.Wp : a.W;
   __amdgpu_buffer_rsrc_t rw[R];
 #pragma unroll
   for (int t = 0; t < R; ++t) {
@@ -312,21 +322,25 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
     if (SILU) {
       const int row0 = (blockIdx.x * (R / 2) + t % (R / 2)) * 16;
       valid = row0 < a.N ? min(16, a.N - row0) : 0;
-      base = static_cast<const bf16_t*>(a.W.ptr[t / (R / 2)]) + static_cast<size_t>(valid ? row0 : 0) * K;
+      base = static_cast<const bf16_t*>(W.ptr[t / (R / 2)]) + static_cast<size_t>(valid ? row0 : 0) * K;
     } else {
       const int row0 = (blockIdx.x * R + t) * 16;
       int b = 0, sg = 0;
-      while (sg < a.W.n_seg - 1 && row0 >= b + a.W.rows[sg]) b += a.W.rows[sg++];
-      valid = row0 < a.N ? min(16, a.W.rows[sg] - (row0 - b)) : 0;
-      base = static_cast<const bf16_t*>(a.W.ptr[sg]) + static_cast<size_t>(valid ? row0 - b : 0) * K;
+      while (sg < W.n_seg - 1 && row0 >= b + W.rows[sg]) b += W.rows[sg++];
+      valid = row0 < a.N ? min(16, W.rows[sg] - (row0 - b)) : 0;
+      base = static_cast<const bf16_t*>(W.ptr[sg]) + static_cast<size_t>(valid ? row0 - b : 0) * K;
     }
-    rw[t] = buffer_rsrc(base, static_cast<uint32_t>(valid) * row_bytes);
+    // a packed tile is whole (16 rows) or absent; a row-major one may be ragged
+    rw[t] = buffer_rsrc(base, static_cast<uint32_t>(PACKED ? (valid ? 16 : 0) : valid) * row_bytes);
   }
   // rows m >= M of the activations read as zeros
   const __amdgpu_buffer_rsrc_t ra =
       buffer_rsrc(a.A, static_cast<uint32_t>(a.M) * static_cast<uint32_t>(a.lda) * 2u);
   const int kb = (u0 + wave) * 128 + g * 32;
-  const int woff = r * static_cast<int>(row_bytes) + kb;
+  // row-major: lane (g, r) reads 32 bytes of row r per unit (two 16-byte pieces), units 128 bytes
+  // apart; packed: the unit's 2 KB run, the lane's 16 bytes in each 1 KB half
+  const int woff = PACKED ? (u0 + wave) * 2048 + lane * 16 : r * static_cast<int>(row_bytes) + kb;
+  constexpr int kWStep = PACKED ? 4 * 2048 : 4 * 128, kWHalf = PACKED ? 1024 : 16;
   int aoff[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) aoff[mt] = (mt * 16 + r) * static_cast<int>(a.lda) * 2 + kb;
@@ -343,11 +357,11 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
   // activations of stage s never waits for weights of later stages.
   bf16x8_t wv[D][R][2], av[MT][2];
   auto load_w = [&](int s, int unit) {
-    const int o = unit * 512;
+    const int o = unit * kWStep;
 #pragma unroll
     for (int t = 0; t < R; ++t) {
-      wv[s][t][0] = load_bf16x8(rw[t], woff + o);
-      wv[s][t][1] = load_bf16x8(rw[t], woff + o + 16);
+      wv[s][t][0] = load_w16<PACKED>(rw[t], woff + o);
+      wv[s][t][1] = load_w16<PACKED>(rw[t], woff + o + kWHalf);
     }
   };
   auto load_a = [&](int unit) {
@@ -785,7 +799,22 @@ void launch_deep_t(const GemmArgs& a, hipStream_t s) {
   const int ups = (KU + a.splits - 1) / a.splits;
   const int per = SILU ? R / 2 : R;
   const int nb = (a.N / 16 + per - 1) / per;
-  launch_kernel((k_gemm_deep<R, MT, D, SILU>), dim3(nb, a.splits), dim3(256), 0, s, a, ups);
+  if (a.Wp.n_seg > 0)
+    launch_kernel((k_gemm_deep<R, MT, D, SILU, true>), dim3(nb, a.splits), dim3(256), 0, s, a, ups);
+  else
+    launch_kernel((k_gemm_deep<R, MT, D, SILU, false>), dim3(nb, a.splits), dim3(256), 0, s, a, ups);
+}
+
+// One thread per 16-byte piece of the packed matrix (the layout of launch_pack_weights).
+__global__ void k_pack_weights(const uint4* __restrict__ w, uint4* __restrict__ p, int rows, int K) {
+  const size_t n = static_cast<size_t>(rows) * K / 8;
+  const size_t tile_pieces = static_cast<size_t>(2) * K;  // 16 rows x K / 8
+  for (size_t q = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; q < n;
+       q += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const size_t t = q / tile_pieces, rem = q % tile_pieces;
+    const int u = static_cast<int>(rem >> 7), j = static_cast<int>(rem >> 6) & 1, l = static_cast<int>(rem) & 63;
+    p[q] = w[((t * 16 + (l & 15)) * static_cast<size_t>(K) + 64 * u + 16 * (l >> 4) + 8 * j) / 8];
+  }
 }
 
 // The (R, D) pairs instantiated for each activation tile count MT = ceil(M / 16).
@@ -917,6 +946,15 @@ GemmPlan plan_gemm(int bf16, int M, int N, int K, bool silu, int max_splits) {
 
 int gemm_pick_splits(int bf16, int M, int N, int K, bool silu, int max_splits) {
   return plan_gemm(bf16, M, N, K, silu, max_splits).splits;
+}
+
+hipError_t launch_pack_weights(const void* w, void* packed, int rows, int K, hipStream_t s) {
+  if (!w || !packed || rows <= 0 || rows % 16 || K <= 0 || K % 64 ||
+      (reinterpret_cast<uintptr_t>(w) | reinterpret_cast<uintptr_t>(packed)) % 16)
+    return hipErrorInvalidValue;
+  launch_kernel(k_pack_weights, dim3(2048), dim3(256), 0, s, static_cast<const uint4*>(w), static_cast<uint4*>(packed),
+                rows, K);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {

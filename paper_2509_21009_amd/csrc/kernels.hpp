@@ -71,12 +71,23 @@ struct GemmArgs {
   int64_t lda;
   int M, N, K;       // N: output columns (for kEpiSiluMul: I, with W = {gate, up})
   WSeg W;
+  WSeg Wp;           // the same segments in the packed layout of launch_pack_weights (n_seg 0: none);
+                     // the decode-regime deep kernel reads them when present
   int epi;
   int splits;        // S >= 1; kEpiSiluMul requires 1
   float* part;       // [S, M, N] (kEpiPartial)
   void* act_out;     // [M, N] dtype T (kEpiSiluMul)
   int variant;       // 0: automatic; 1 stream, 2/3 skinny (16/32 rows per wave), 4 tiled, 6 deep
 };
+
+// Packed weight layout for the decode GEMM (bf16, rows % 16 == 0, K % 64 == 0):
+// 16-byte piece [t][u][j][l] = W[16t + (l & 15)][64u + 16(l >> 4) + 8j .. + 8],
+// for row tile t, 64-wide K unit u, half j and lane l.  A (tile, unit) pair is
+// one contiguous 2 KB run, and each half of it is the 1 KB that one wave
+// instruction loads: lane l gets exactly the MFMA operand it reads from the
+// row-major matrix, so the products are unchanged.  Tile t starts at byte
+// 32 t K, where row 16t starts in the row-major matrix.
+hipError_t launch_pack_weights(const void* w, void* packed, int rows, int K, hipStream_t s);
 
 // Picks the kernel from dtype, M, N and K.  Returns hipSuccess or a launch error.
 hipError_t launch_gemm(int dtype_bf16, const GemmArgs& a, hipStream_t s);

@@ -137,6 +137,18 @@ void rp_engine_destroy(rp_engine* eng) {
   delete eng;
 }
 
+rp_status rp_packed_weights_bytes(const rp_model_config* cfg, size_t* bytes) {
+  return guarded([&] {
+    if (!cfg || !bytes) throw rollpack::RpError(RP_ERR_INVALID_ARG, "null argument");
+    rollpack::validate_config(*cfg);
+    *bytes = rollpack::packed_weights_bytes(*cfg);
+  });
+}
+
+rp_status rp_engine_set_packed_weights(rp_engine* eng, void* packed_ws, size_t bytes) {
+  return engine_call(eng, [&](rollpack::Engine* e) { e->set_packed_weights(packed_ws, bytes); });
+}
+
 rp_status rp_prefill(rp_engine* eng, int32_t n, const int64_t* seq_ids, const int32_t* prompt_tokens,
                      const int64_t* prompt_offsets, const int32_t* max_new_tokens, uint64_t seed, float temperature,
                      float* logits_out, int32_t* first_tokens_out) {

@@ -104,6 +104,8 @@ SIGNATURES = {
                                         ctypes.POINTER(RpEngineLimits), _P, ctypes.c_size_t, _P, ctypes.c_size_t,
                                         _P, ctypes.POINTER(_P)]),
     "rp_engine_destroy": (None, [_P]),
+    "rp_packed_weights_bytes": (ctypes.c_int, [ctypes.POINTER(RpModelConfig), _SZP]),
+    "rp_engine_set_packed_weights": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
     "rp_prefill": (ctypes.c_int, [_P, ctypes.c_int32, _I64P, _I32P, _I64P, _I32P, ctypes.c_uint64, ctypes.c_float,
                                   _P, _I32P]),
     "rp_decode_step": (ctypes.c_int, [_P, _I32P, _P, _I64P, _I32P]),
@@ -202,6 +204,16 @@ def rp_engine_create(cfg, weights: RpWeights, limits, kv_ptr: int, kv_bytes: int
 
 def rp_engine_destroy(eng: int) -> None:
     load_library().rp_engine_destroy(eng)
+
+
+def rp_packed_weights_bytes(cfg: RpModelConfig) -> int:
+    b = ctypes.c_size_t()
+    _check(load_library().rp_packed_weights_bytes(ctypes.byref(cfg), ctypes.byref(b)))
+    return b.value
+
+
+def rp_engine_set_packed_weights(eng: int, ptr: Optional[int], nbytes: int) -> None:
+    _check(load_library().rp_engine_set_packed_weights(eng, ptr, nbytes))
 
 
 def rp_prefill(eng: int, seq_ids, prompt_tokens, prompt_offsets, max_new_tokens, seed: int, temperature: float,
@@ -479,10 +491,12 @@ class Engine:
     weights: dict with "embed", "final_norm", "lm_head" (None if tied) and
     "layers" (list of dicts with the rp_layer_weights field names), all
     contiguous device tensors of the model dtype.  The dict is kept alive.
+    pack_weights: for a bf16 model, also allocate the packed copy of the
+    weights that the decode GEMMs stream (rp_engine_set_packed_weights).
     """
 
     def __init__(self, shape, weights: dict, max_seqs: int, max_prefill_tokens: int, max_context: int,
-                 kv_pages: int, stream=None):
+                 kv_pages: int, stream=None, pack_weights: bool = True):
         import torch
         self.torch = torch
         self.shape = shape
@@ -498,6 +512,11 @@ class Engine:
         self.handle = rp_engine_create(self.cfg, self._w, self.limits, self.kv.data_ptr(), kv_bytes,
                                        self.scratch.data_ptr(), sc_bytes, self.stream.cuda_stream)
         self.max_seqs = max_seqs
+        self.packed = None
+        if pack_weights and shape.dtype == "bf16":
+            nbytes = rp_packed_weights_bytes(self.cfg)
+            self.packed = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+            rp_engine_set_packed_weights(self.handle, self.packed.data_ptr(), nbytes)
 
     def close(self):
         if getattr(self, "handle", None):

@@ -85,6 +85,16 @@ def test_workspace_size_and_kv_bytes(lib):
     assert rp.rp_workspace_size(cfg, lim2)[0] == 2 * kv
 
 
+def test_packed_weights_bytes(lib):
+    """The packed copy holds every projection and the LM head once (for these shapes every
+    tensor is already a multiple of 256 bytes); the fp32 model has none."""
+    for name in ("qwen2.5-7b", "qwen2.5-0.5b", "qwen2.5-32b"):
+        s = SHAPES[name]
+        per_layer = s.hidden * s.qkv_out + s.n_q * s.head_dim * s.hidden + 3 * s.hidden * s.inter
+        assert rp.rp_packed_weights_bytes(rp.model_config(s)) == 2 * (s.layers * per_layer + s.vocab * s.hidden)
+    assert rp.rp_packed_weights_bytes(rp.model_config(SHAPES["tiny"])) == 0
+
+
 @pytest.mark.parametrize("field,value", [("head_dim", 96), ("n_kv_heads", 3), ("hidden", 100), ("vocab", 1000)])
 def test_invalid_configs_are_rejected(lib, field, value):
     import dataclasses

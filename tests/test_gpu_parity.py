@@ -332,3 +332,35 @@ def test_stream_read_ceiling():
     with pytest.raises(R.RollpackError):
         R.rp_stream_read_gbs(torch.zeros(1024, dtype=torch.int32, device=DEV), 1)
 
+
+
+def test_packed_weights_give_identical_logits():
+    """The decode GEMMs read a packed copy of the weights when the engine has one
+    (rp_engine_set_packed_weights); every lane loads the same MFMA operand as from the
+    row-major matrix, so prefill and teacher-forced decode logits must be bitwise equal with
+    and without it, over the deep kernel's regimes (1-4 activation tiles, K-split down and
+    q/k/v projections, a ragged LM head of 8,320 rows) at the 7B layer shape."""
+    R = rp()
+    s = truncated(SHAPES["qwen2.5-7b"], 2, vocab=8320)
+    wd = make_weights(s, seed=2, device=DEV)
+    rng = np.random.default_rng(9)
+    for B in (1, 17, 40, 64):
+        plen = rng.integers(1, 40, size=B)
+        toks = rng.integers(0, s.vocab, size=int(plen.sum())).astype(np.int32)
+        offs = np.concatenate([[0], np.cumsum(plen)]).astype(np.int64)
+        ids = np.arange(10, 10 + B, dtype=np.int64)
+        forced = rng.integers(0, s.vocab, size=(3, B)).astype(np.int32)
+        out = []
+        for pack in (True, False):
+            eng = R.Engine(s, R.weights_for_engine(wd), max_seqs=64, max_prefill_tokens=4096, max_context=64,
+                           kv_pages=2 * 64, pack_weights=pack)
+            assert (eng.packed is not None) == pack
+            lg0, _ = eng.prefill(ids, toks, offs, np.full(B, 4, np.int32), 3, 1.0, logits=True)
+            rows = [lg0.cpu().numpy()]
+            for j in range(3):
+                _, _, lg = eng.decode_step(forced_tokens=forced[j], logits=True)
+                rows.append(lg.cpu().numpy())
+            out.append(np.stack(rows))
+            eng.close()
+        log(f"packed vs row-major weights, B={B}: identical={np.array_equal(out[0], out[1])}")
+        assert np.array_equal(out[0], out[1]), B
