@@ -219,11 +219,13 @@ def gemm_rates(eng, wl):
     live, the sequences then aborted.  flops are 2*M*N*K per launch, bytes the algorithmic
     weights + activations + outputs."""
     import torch
-    eng.profile(PREFILL_GEMMS)
+    eng.profile(PREFILL_GEMMS + ["attn"])
     eng.prefill(wl.seq_ids, wl.prompt_tokens, wl.prompt_offsets, np.maximum(wl.max_new, 2).astype(np.int32),
                 wl.sample_seed, wl.temperature)
     torch.cuda.synchronize()
-    prof = [p for p in eng.profile_read() if p["phase"] == "prefill" and p["kernel"] in PREFILL_GEMMS]
+    allp = eng.profile_read()
+    prof = [p for p in allp if p["phase"] == "prefill" and p["kernel"] in PREFILL_GEMMS]
+    attn = [p for p in allp if p["phase"] == "prefill" and p["kernel"] == "attn"]
     eng.profile(DECODE_GEMMS)
     # steps before the first sequence could finish, so the batch stays whole
     steps = max(1, min(FULL_BATCH_DECODE_STEPS, int(np.maximum(wl.max_new, 2).min()) - 1))
@@ -253,7 +255,11 @@ def gemm_rates(eng, wl):
     if full is not None:
         full["rows"] = int(wl.n)
         full["steps"] = steps
-    return pre, full
+    att = rates(attn)
+    if att is not None:
+        att.pop("per_kernel_tflops", None)
+        att["flops"] = "2 n_q hd sum_i p_i(p_i + 1): the causal products only"
+    return pre, full, att
 
 
 def warmup_steps(eng, wl, n_steps):
@@ -402,7 +408,8 @@ def main():
         roof["frac_measured"] = round(roof["achieved"] / stream, 4)
     if shape.dtype == "bf16" and not args.no_gemm_rates:
         t0 = time.perf_counter()
-        out["config"]["prefill_gemm_mfma"], out["config"]["decode_gemm_full_batch"] = gemm_rates(eng, wl)
+        (out["config"]["prefill_gemm_mfma"], out["config"]["decode_gemm_full_batch"],
+         out["config"]["prefill_attn_mfma"]) = gemm_rates(eng, wl)
         log(f"GEMM rate pass in {time.perf_counter() - t0:.1f} s")
     if args.compare_unscheduled and wl.round_id is not None:
         log("running the same sequences as one unscheduled batch")

@@ -1,8 +1,7 @@
 // Causal GQA attention over the paged KV cache.
 //
-// One 64-lane wave owns a work item: up to 16 query rows that share one KV
-// head (the G query heads of a token, or G heads x floor(16/G) tokens in
-// prefill) and a range of KV tokens.  Per 32-token half page it computes
+// Decode: one 64-lane wave owns a work item: the G query heads of a token
+// (up to 16 query rows that share one KV head) and a range of KV tokens.  Per 32-token half page it computes
 // S^T = K Q^T as two 16x16 MFMA tiles, runs an online softmax in the log2
 // domain, and accumulates O^T = V^T P^T with MFMA.  Both operands are read
 // as 16-byte pieces straight from HBM, each load instruction one contiguous
@@ -13,6 +12,9 @@
 // are exactly the P^T operand it must supply, with no data exchange between
 // lanes.
 //
+// Prefill stages each K/V page in LDS once per block of query tokens
+// (k_attn_prefill_lds below); its waves run the same page step from LDS.
+//
 // Decode splits each sequence's context into chunks (one work item each, with
 // a host-built descriptor) so that small batches with long contexts still
 // spread over all CUs; the half pages of an item stream through a ring of
@@ -20,6 +22,7 @@
 // partial outputs.
 #include "device_common.hpp"
 #include "kernels.hpp"
+#include "lds_dma.hpp"
 
 namespace rollpack {
 
@@ -36,78 +39,6 @@ struct SoftmaxState {
   float m, l;
 };
 
-// Process one page for the 16 rows of a wave.  qf: query operands;
-// row_lim: last key position row c may see (inclusive); t_lo/t_hi: the
-// item's key range [t_lo, t_hi).
-template <int HD>
-__device__ __forceinline__ void attend_page(const bf16_t* kb, const bf16_t* vb, int page_tok0,
-                                            const bf16x8_t (&qf)[HD / 32], int row_lim, int t_lo,
-                                            int t_hi, float scale_log2, SoftmaxState& st,
-                                            f32x4_t (&o)[HD / 16]) {
-  constexpr int KS = HD / 32;
-  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
-  f32x4_t sacc[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    // tile t = 2h + tt of the page: its k-step ks is the 1 KB run (t * KS + ks), lane (g, c) at (4c + g) * 8
-    const bf16_t* krow = kb + (t * KS * 16 + c) * 32 + g * 8;
-    bf16x8_t kf[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf[ks] = load_bf16x8(krow + ks * 512);
-    sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) sacc[t] = mfma16x16x32(kf[ks], qf[ks], sacc[t]);
-  }
-  bf16x8_t vf[HD / 16][2];
-#pragma unroll
-  for (int blk = 0; blk < HD / 16; ++blk)
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp) vf[blk][pp] = load_bf16x8(vb + pp * HD * 32 + (blk * 16 + c) * 32 + 8 * g);
-
-  float sv[16];
-  float pmax = -INFINITY;
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int tok = page_tok0 + 32 * (t >> 1) + 8 * g + 4 * (t & 1) + e;
-      float v = sacc[t][e] * scale_log2;
-      if (tok < t_lo || tok >= t_hi || tok > row_lim) v = -INFINITY;
-      sv[t * 4 + e] = v;
-      pmax = fmaxf(pmax, v);
-    }
-  pmax = fmaxf(pmax, __shfl_xor(pmax, 16, 64));
-  pmax = fmaxf(pmax, __shfl_xor(pmax, 32, 64));
-  const float m_new = fmaxf(st.m, pmax);
-  const float shift = (m_new == -INFINITY) ? 0.f : m_new;
-  const float alpha = exp2f(st.m - shift);
-  float psum = 0.f;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    sv[i] = exp2f(sv[i] - shift);
-    psum += sv[i];
-  }
-  psum += __shfl_xor(psum, 16, 64);
-  psum += __shfl_xor(psum, 32, 64);
-  st.l = st.l * alpha + psum;
-  st.m = m_new;
-  bf16x8_t pf[2];
-#pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
-    uint4 w;
-    w.x = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 0])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 1])) << 16);
-    w.y = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 2])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 3])) << 16);
-    w.z = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 4])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 5])) << 16);
-    w.w = static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 6])) | (static_cast<uint32_t>(f32_to_bf16(sv[pp * 8 + 7])) << 16);
-    pf[pp] = __builtin_bit_cast(bf16x8_t, w);
-  }
-#pragma unroll
-  for (int blk = 0; blk < HD / 16; ++blk) {
-    o[blk] = o[blk] * alpha;
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp) o[blk] = mfma16x16x32(vf[blk][pp], pf[pp], o[blk]);
-  }
-}
 
 // A 16-byte load marked non-temporal, for the KV cache that a decode step
 // streams exactly once: the caches then do not keep it at the expense of
@@ -394,62 +325,250 @@ __global__ __launch_bounds__(64) void k_attn_merge_few(AttnArgs a) {
   for (int k = 0; k < NPL; ++k) out[64 * k] = f32_to_bf16(tn[k] / td);
 }
 
-template <int HD>
-__global__ __launch_bounds__(64) void k_attn_prefill_bf16(AttnArgs a, int tpi) {
+// Prefill attention with K/V pages staged in LDS and shared by a block.
+//
+// A block of 8 waves owns one KV head and kPrefillWaveGroups * 8 query groups
+// of one sequence piece; a query group is the G query heads of tpi = 16 / G
+// consecutive tokens (one 16-column MFMA operand), and each wave holds
+// kPrefillWaveGroups of them.  The block walks the causal prefix one 64-token
+// page at a time: the page's K and V blocks (copied unchanged from the cache,
+// with each 1 KB run reordered so that a wave's read of it is 64 consecutive
+// 16-byte pieces) pass through a two-stage LDS ring filled by LDS-DMA
+// copies one page ahead, and every wave runs the decode kernel's page step (S^T = K Q^T, online
+// softmax in the log2 domain, O^T += V^T P^T) on them for its groups, each K
+// and V fragment read once for all of its groups.  The global K/V traffic of
+// a prefix is then paid once per block instead of once per group.  Two blocks
+// share a CU (under 128 registers per lane and 72 KB of LDS each), so one
+// block's barriers and the dependent S -> softmax -> PV chain of its waves
+// overlap with the other's MFMAs: measured on the 7B short round's prefill,
+// 0.16 of the dense bf16 peak against 0.12 with two groups per wave and one
+// block per CU, and 0.14 with 16 waves per block.
+constexpr int kPrefillWaveGroups = 1;
+constexpr int kPrefillWaves = 8;
+constexpr int kMaxContextPages = 65536 / kPageTokens;  // the engine's context limit
+
+typedef __bf16 bf16x2_hw __attribute__((ext_vector_type(2)));
+typedef float f32x2_hw __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to packed bf16, round to nearest even (gfx950's v_cvt_pk_bf16_f32; for the
+// finite values here the same result as f32_to_bf16).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_hw{lo, hi}, bf16x2_hw));
+}
+
+// One page step of the prefill kernel for a wave's NG query groups.  masked: whether any key
+// of the page lies past some column's own position (the diagonal pages); the others need no mask.
+// Exponents go through the bare v_exp_f32: their arguments are <= 0, and results below 2^-126,
+// which it flushes, are far below what bf16 probabilities resolve.
+template <int HD, int NG>
+__device__ __forceinline__ void attend_page_lds(const bf16_t* kb, const bf16_t* vb, int page_tok0, bool masked,
+                                                const bf16x8_t (&qf)[NG][HD / 32], const int (&row_lim)[NG],
+                                                float scale_log2, SoftmaxState (&st)[NG],
+                                                f32x4_t (&o)[NG][HD / 16]) {
   constexpr int KS = HD / 32;
-  const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  // LDS holds each 1 KB run of the page lane-ordered (the page copies of k_attn_prefill_lds): lane l
+  // reads piece l of a run.
+  const bf16x8_t* kr = reinterpret_cast<const bf16x8_t*>(kb) + lane;
+  const bf16x8_t* vr = reinterpret_cast<const bf16x8_t*>(vb) + lane;
+  f32x4_t sacc[NG][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    bf16x8_t kf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = kr[(t * KS + ks) * 64];
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      sacc[q][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) sacc[q][t] = mfma16x16x32(kf[ks], qf[q][ks], sacc[q][t]);
+    }
+  }
+  bf16x8_t pf[NG][2];
+  float alpha[NG];
+#pragma unroll
+  for (int q = 0; q < NG; ++q) {
+    float sv[16];
+    float pmax = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float v = sacc[q][t][e] * scale_log2;
+        if (masked && page_tok0 + 32 * (t >> 1) + 8 * g + 4 * (t & 1) + e > row_lim[q]) v = -INFINITY;
+        sv[t * 4 + e] = v;
+        pmax = fmaxf(pmax, v);
+      }
+    pmax = fmaxf(pmax, __shfl_xor(pmax, 16, 64));
+    pmax = fmaxf(pmax, __shfl_xor(pmax, 32, 64));
+    const float m_new = fmaxf(st[q].m, pmax);
+    const float shift = (m_new == -INFINITY) ? 0.f : m_new;
+    alpha[q] = __builtin_amdgcn_exp2f(st[q].m - shift);
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      sv[i] = __builtin_amdgcn_exp2f(sv[i] - shift);
+      psum += sv[i];
+    }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    st[q].l = st[q].l * alpha[q] + psum;
+    st[q].m = m_new;
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      uint4 w;
+      w.x = pack_bf16x2(sv[pp * 8 + 0], sv[pp * 8 + 1]);
+      w.y = pack_bf16x2(sv[pp * 8 + 2], sv[pp * 8 + 3]);
+      w.z = pack_bf16x2(sv[pp * 8 + 4], sv[pp * 8 + 5]);
+      w.w = pack_bf16x2(sv[pp * 8 + 6], sv[pp * 8 + 7]);
+      pf[q][pp] = __builtin_bit_cast(bf16x8_t, w);
+    }
+  }
+#pragma unroll
+  for (int blk = 0; blk < HD / 16; ++blk) {
+    bf16x8_t vf[2];
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) vf[pp] = vr[(pp * HD / 16 + blk) * 64];
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      o[q][blk] = o[q][blk] * alpha[q];
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp) o[q][blk] = mfma16x16x32(vf[pp], pf[q][pp], o[q][blk]);
+    }
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill_lds(AttnArgs a, int tpi) {
+  constexpr int KS = HD / 32, NG = kPrefillWaveGroups;
+  constexpr int PAGE_EL = kPageTokens * HD;                 // elements of one (page, head) K or V block
+  constexpr int RUNS = 2 * PAGE_EL * 2 / 1024;              // 1 KB runs of a page's K and V blocks
+  constexpr int DPW = RUNS / kPrefillWaves;                 // runs each wave copies per page
+  constexpr int NST = 2, AHEAD = NST - 1;                   // LDS stages; pages in flight
+  static_assert(RUNS % kPrefillWaves == 0, "page staging");
+  constexpr int NT = 64 * kPrefillWaves;
+  __shared__ __attribute__((aligned(1024))) bf16_t kv[NST][2 * PAGE_EL];  // [stage][K block, V block]
+  __shared__ int s_off[NT];                                           // item offsets of the chunk's pieces
+  __shared__ int s_pt[kMaxContextPages];                              // the piece's page-table row
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  const int wave = threadIdx.x >> 6;
   const int x = blockIdx.x, kh = blockIdx.y;
+  // Which piece the block serves: one cooperative load of the item offsets into LDS, then a
+  // search there (a global binary search would chain its loads' latencies).
+  const int n_cached = min(a.n_seq + 1, NT);
+  if (static_cast<int>(threadIdx.x) < n_cached) s_off[threadIdx.x] = a.item_off[threadIdx.x];
+  __syncthreads();
   int lo = 0, hi = a.n_seq;
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
-    if (a.item_off[mid] <= x) lo = mid; else hi = mid;
+    if ((mid < n_cached ? s_off[mid] : a.item_off[mid]) <= x) lo = mid; else hi = mid;
   }
   const int j = lo;
-  const int qb = x - a.item_off[j];
+  // the piece's blocks in reverse: later query tokens attend to more pages, so they start first
+  const int n_blk = (j + 1 < n_cached ? s_off[j + 1] : a.item_off[j + 1]) - (j < n_cached ? s_off[j] : a.item_off[j]);
+  const int qb = n_blk - 1 - (x - (j < n_cached ? s_off[j] : a.item_off[j]));
   const int ntok = a.seq_ntok[j];
   const int G = a.n_q / a.n_kv;
-  const int tq = qb * tpi + c / G;
-  const bool valid = c < tpi * G && tq < ntok;
-  const int head = kh * G + c % G;
   const int pos0 = a.seq_pos0[j];
-  const int row_lim = valid ? pos0 + tq : -1;
-  const int last_tok = min(qb * tpi + tpi, ntok) - 1;
-  const int t_end = pos0 + last_tok + 1;
-  const size_t qrow_idx = static_cast<size_t>(a.seq_row0[j] + tq);
+  const int block_tok = kPrefillWaves * NG * tpi;
+  const int last_tok = min(qb * block_tok + block_tok, ntok) - 1;
+  const int t_end = pos0 + last_tok + 1;  // keys the block needs: [0, t_end)
 
-  bf16x8_t qf[KS];
-  if (valid) {
-    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + (qrow_idx * a.n_q + head) * HD + g * 8;
+  // this lane's query column in each of the wave's groups
+  bf16x8_t qf[NG][KS];
+  int row_lim[NG], tq[NG], head = kh * G + c % G;
+  bool valid[NG];
+  int wave_lim = -1, wave_min = 1 << 30;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + ks * 32);
-  } else {
+  for (int q = 0; q < NG; ++q) {
+    tq[q] = qb * block_tok + (wave * NG + q) * tpi + c / G;
+    valid[q] = c < tpi * G && tq[q] < ntok;
+    row_lim[q] = valid[q] ? pos0 + tq[q] : -1;
+    wave_lim = max(wave_lim, row_lim[q]);
+    if (valid[q]) wave_min = min(wave_min, row_lim[q]);
+    if (valid[q]) {
+      const bf16_t* qrow = static_cast<const bf16_t*>(a.q) +
+                           ((static_cast<size_t>(a.seq_row0[j] + tq[q])) * a.n_q + head) * HD + g * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
+      for (int ks = 0; ks < KS; ++ks) qf[q][ks] = load_bf16x8(qrow + ks * 32);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[q][ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
+    }
   }
-  f32x4_t o[HD / 16];
 #pragma unroll
-  for (int blk = 0; blk < HD / 16; ++blk) o[blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  SoftmaxState st{-INFINITY, 0.f};
+  for (int m = 32; m >= 1; m >>= 1) {  // the wave's last and first query positions
+    wave_lim = max(wave_lim, __shfl_xor(wave_lim, m, 64));
+    wave_min = min(wave_min, __shfl_xor(wave_min, m, 64));
+  }
+  f32x4_t o[NG][HD / 16];
+  SoftmaxState st[NG];
+#pragma unroll
+  for (int q = 0; q < NG; ++q) {
+    st[q] = SoftmaxState{-INFINITY, 0.f};
+#pragma unroll
+    for (int blk = 0; blk < HD / 16; ++blk) o[q][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
   const bf16_t* kpool = static_cast<const bf16_t*>(a.k_pool);
   const bf16_t* vpool = static_cast<const bf16_t*>(a.v_pool);
   const float scale_log2 = a.scale * kLog2e;
-  const int* pt = a.page_table + static_cast<size_t>(a.seq_slot[j]) * a.pt_stride;
-  for (int p = 0; p * kPageTokens < t_end; ++p) {
-    const size_t pb = (static_cast<size_t>(pt[p]) * a.n_kv + kh) * kPageTokens * HD;
-    attend_page<HD>(kpool + pb, vpool + pb, p * kPageTokens, qf, row_lim, 0, t_end, scale_log2, st, o);
+  const int npages = (t_end + kPageTokens - 1) / kPageTokens;  // <= kMaxContextPages (max_context <= 65536)
+  {
+    const int* ptg = a.page_table + static_cast<size_t>(a.seq_slot[j]) * a.pt_stride;
+    for (int i = threadIdx.x; i < npages; i += NT) s_pt[i] = ptg[i];
   }
-  if (valid) {
-    const float inv = 1.0f / st.l;
-    bf16_t* out = static_cast<bf16_t*>(a.out) + (qrow_idx * a.n_q + head) * HD;
+  __syncthreads();
+  const int* pt = s_pt;
+
+  // Pages go from the cache straight into LDS (buffer_load ... lds, no register staging), AHEAD
+  // pages ahead of the one being computed; wave w copies runs w, w + 8, ... of each page.  Within
+  // a run, LDS piece 16g + c receives the cache's piece 4c + g, the one lane 16g + c reads, so a
+  // wave's 64 lanes read 64 consecutive LDS pieces, free of bank conflicts.  Past the last page the
+  // copies repeat it, so that every iteration waits for the same number of loads (the extra
+  // copies land in stages nobody reads again).
+  typedef const __attribute__((address_space(3))) char lds_char;
+  const uint32_t lds_kv = static_cast<uint32_t>((uintptr_t)(lds_char*)(&kv[0][0]));  // LDS byte address
+  const int lane_src = 16 * (((lane & 15) << 2) | (lane >> 4));
+  auto issue = [&](int page, int stage) {
+    const int pg = __builtin_amdgcn_readfirstlane(pt[page]);
+    const size_t pb = (static_cast<size_t>(pg) * a.n_kv + kh) * PAGE_EL;
+    const u32x4_raw kres = raw_rsrc(kpool + pb, PAGE_EL * 2), vres = raw_rsrc(vpool + pb, PAGE_EL * 2);
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const int run = wave + kPrefillWaves * i;  // runs below RUNS / 2 are K, the rest V
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_kv + static_cast<uint32_t>(stage * PAGE_EL * 4 + run * 1024));
+      if (run < RUNS / 2)
+        dma16(kres, dst, run * 1024 + lane_src);
+      else
+        dma16(vres, dst, (run - RUNS / 2) * 1024 + lane_src);
+    }
+  };
+#pragma unroll
+  for (int s0 = 0; s0 < AHEAD; ++s0) issue(min(s0, npages - 1), s0);
+  for (int p = 0; p < npages; ++p) {
+    wait_vmcnt<(AHEAD - 1) * DPW>();  // this wave's copies of page p have landed
+    __syncthreads();                  // every wave's have; every wave is done with page p - 1
+    issue(min(p + AHEAD, npages - 1), (p + AHEAD) % NST);  // into the stage that held page p - 1
+    if (p * kPageTokens <= wave_lim)
+      attend_page_lds<HD, NG>(kv[p % NST], kv[p % NST] + PAGE_EL, p * kPageTokens,
+                              p * kPageTokens + kPageTokens - 1 > wave_min, qf, row_lim, scale_log2, st, o);
+  }
+
+#pragma unroll
+  for (int q = 0; q < NG; ++q) {
+    if (!valid[q]) continue;
+    const float inv = 1.0f / st[q].l;
+    bf16_t* out = static_cast<bf16_t*>(a.out) + ((static_cast<size_t>(a.seq_row0[j] + tq[q])) * a.n_q + head) * HD;
 #pragma unroll
     for (int blk = 0; blk < HD / 16; ++blk) {
       uint2 pk;
-      pk.x = static_cast<uint32_t>(f32_to_bf16(o[blk][0] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[blk][1] * inv)) << 16);
-      pk.y = static_cast<uint32_t>(f32_to_bf16(o[blk][2] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[blk][3] * inv)) << 16);
+      pk.x = static_cast<uint32_t>(f32_to_bf16(o[q][blk][0] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[q][blk][1] * inv)) << 16);
+      pk.y = static_cast<uint32_t>(f32_to_bf16(o[q][blk][2] * inv)) | (static_cast<uint32_t>(f32_to_bf16(o[q][blk][3] * inv)) << 16);
       *reinterpret_cast<uint2*>(out + blk * 16 + 4 * g) = pk;
     }
   }
 }
+
 
 // fp32 model: one wave per (row, query head), one key at a time.
 __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
@@ -487,10 +606,15 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
 
 }  // namespace
 
-int attn_prefill_tokens_per_item(int bf16, int group) {
-  if (!bf16) return 1;
+// Query tokens of one 16-column MFMA group: the G heads of each token side by side.
+static int prefill_group_tokens(int group) {
   const int t = 16 / group;
   return t < 1 ? 1 : t;
+}
+
+int attn_prefill_tokens_per_item(int bf16, int group) {
+  if (!bf16) return 1;
+  return kPrefillWaves * kPrefillWaveGroups * prefill_group_tokens(group);
 }
 
 hipError_t launch_attn_decode(int bf16, const AttnArgs& a, hipStream_t s) {
@@ -541,10 +665,10 @@ hipError_t launch_attn_prefill(int bf16, const AttnArgs& a, hipStream_t s) {
   if (a.total_items <= 0) return hipSuccess;
   const int G = a.n_q / a.n_kv;
   if (G > 16) return hipErrorInvalidValue;
-  const int tpi = attn_prefill_tokens_per_item(1, G);
+  const int tpi = prefill_group_tokens(G);
   dim3 grid(a.total_items, a.n_kv);
-  if (a.hd == 128) launch_kernel(k_attn_prefill_bf16<128>, grid, dim3(64), 0, s, a, tpi);
-  else if (a.hd == 64) launch_kernel(k_attn_prefill_bf16<64>, grid, dim3(64), 0, s, a, tpi);
+  if (a.hd == 128) launch_kernel(k_attn_prefill_lds<128>, grid, dim3(64 * kPrefillWaves), 0, s, a, tpi);
+  else if (a.hd == 64) launch_kernel(k_attn_prefill_lds<64>, grid, dim3(64 * kPrefillWaves), 0, s, a, tpi);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
