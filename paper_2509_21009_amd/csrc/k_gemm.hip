@@ -483,9 +483,13 @@ __global__ __launch_bounds__(256) void k_gemm_deep(GemmArgs a, int units_per_spl
 // eight distinct 16-byte bank groups.  Rows past M or N read as zeros
 // through the buffer resources (range-checked loads); a 16-row block of a
 // weight tile lies in one weight segment.  Each XCD takes a contiguous run
-// of the tile order (block ids equal mod 8), and the order walks gm m tiles
-// of one weight panel before the next panel, so the 32 tiles an XCD runs at
-// once share gm activation tiles and 32 / gm weight panels in its L2.  gm is
+// of the (split, tile) order, split-major (block ids equal mod 8), and the
+// order walks gm m tiles of one weight panel before the next panel, so the
+// 32 tiles an XCD runs at once share gm activation tiles and 32 / gm weight
+// panels in its L2.  (A run per tile with the split on blockIdx.y gave one XCD
+// every split of its tiles: at 129-256 rows the down projection's 28 panels x 9
+// splits put 36 blocks on each of seven XCDs, two rounds, and none on the
+// eighth; balanced, it runs in 49 against 93 us at 256 rows.)  gm is
 // 8 for wide products (>= 64 panels: gate/up, the LM head) and 2 for
 // narrow ones (measured: at 4k-16k rows gate/up gains 4 points of MFMA peak
 // over a single panel at a time, q/k/v, o and down 2-4).
@@ -512,14 +516,20 @@ __global__ __launch_bounds__(512) void k_gemm_tiled(GemmArgs a, int kblocks_per_
   constexpr int NA = BM / 128, NW = BN / 128;   // 16-row blocks of activations / weights a wave loads per stage
   static_assert(MT >= 1 && (BN == 128 || BN == 256), "tile shape");
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kGNST * STAGE];
+  // Work items are (split, tile) pairs, split-major, and each XCD takes a contiguous run of
+  // them (block ids equal mod 8 run on one XCD): the XCDs get equal shares of a split launch
+  // (per-tile runs would hand one XCD all splits of its tiles, more blocks than its 32 CUs
+  // when the tile count is not a multiple of 8), and an XCD's blocks read few K ranges of
+  // the activations, which its L2 then holds.
   const int n_tiles = n_mb * n_nb;
-  const int per_xcd = (n_tiles + 7) / 8;
-  const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (t >= n_tiles) return;  // block-uniform: padding of the XCD-ordered grid
+  const int n_items = n_tiles * a.splits;
+  const int per_xcd = (n_items + 7) / 8;
+  const int q = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (q >= n_items) return;  // block-uniform: padding of the XCD-ordered grid
+  const int split = q / n_tiles, t = q - split * n_tiles;
   // Grouped order: consecutive tiles walk gm m tiles of one weight panel, then the next panel.
   const int gsz = gm * n_nb, grp = t / gsz, first = grp * gm, gcur = min(gm, n_mb - first);
   const int mb = first + (t - grp * gsz) % gcur, nb = (t - grp * gsz) / gcur;
-  const int split = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WMW, wn = wave / WMW;
@@ -968,9 +978,9 @@ hipError_t launch_gemm(int bf16, const GemmArgs& a, hipStream_t s) {
     const int kbps = (a.K / kGBK + a.splits - 1) / a.splits;
     const int n_nb = silu ? a.N / (bn / 2) : (a.N + bn - 1) / bn;
     const int n_mb = (a.M + bm - 1) / bm;
-    const int per_xcd = (n_mb * n_nb + 7) / 8;
+    const int per_xcd = (n_mb * n_nb * a.splits + 7) / 8;
     const int gm = n_nb >= 64 ? 8 : 2;
-    dim3 grid(8 * per_xcd, a.splits);
+    dim3 grid(8 * per_xcd);
 #define RP_TILED(BM_, BN_)                                                                                   \
     if (bm == BM_ && bn == BN_) {                                                                            \
       if (silu) launch_kernel((k_gemm_tiled<BM_, BN_, true>), grid, dim3(512), 0, s, a, kbps, n_mb, n_nb, gm); \
