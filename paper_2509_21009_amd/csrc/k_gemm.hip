@@ -902,6 +902,17 @@ GemmPlan plan_tiled(int M, int N, int K, bool silu, int max_splits) {
       best = GemmPlan{kKTiled, s, 0, 0, bm, bn};
     }
   }
+  // Two corrections the cost model misses, from a sweep of every tile shape and split at
+  // 96-512 rows of the 7B projections (times with the partial sums included):
+  //  * a product that needs no split (the LM head) takes the 256-row weight panels, as long
+  //    as they still fill the CUs: the 128-row panels only pay for halving a split (LM head
+  //    at 448 / 512 rows: 663 / 716 against 725 / 789 us);
+  //  * gate/up over two 256-row activation tiles (257-512 rows) takes 128-row weight panels:
+  //    592 tiles at two per CU spread the work past one round more evenly than 296 at one per
+  //    CU (155 / 167 against 178 / 188 us at 448 / 512 rows).
+  const int n_mb = (M + best.bm - 1) / best.bm;
+  if (!silu && best.bn == 128 && best.splits == 1 && ((N + 255) / 256) * n_mb >= 256) best.bn = 256;
+  if (silu && M <= 512 && best.bm == 256 && n_mb >= 2) best.bn = 128;
   best.splits = even_splits(KB, std::min(best.splits, max_splits));
   return best;
 }
