@@ -875,44 +875,56 @@ GemmPlan plan_deep(int M, int N, int K, bool silu, int max_splits) {
 // k_gemm_tiled plan: the block tile (BM activation rows x BN weight rows) and
 // the K split.  A block holds one CU's LDS ring and the 8 waves of two
 // SIMD-pairs, so the time is set by rounds of 256 blocks times the K steps of
-// one block; per K step a BM = 128 block takes 0.71 of a BM = 256 block
-// (measured at 4k rows on the 7B shapes).  The smaller tile pays where it
-// saves padded rows or a round: 65-128 and 257-384 rows of the gate/up
-// projection, for instance.  Non-SiLU products split K until the blocks fill
-// one round, keeping >= 8 K steps per split.  At decode batches (<= 512 rows)
-// they take 128-row weight panels: twice the panels for the same blocks, so
-// half the split and half its fp32 partial traffic, which at these sizes
-// exceeds the weights themselves (q/k/v at 256 rows and 14 splits: 66 MB of
-// partials for 33 MB of weights); measured 1.15-1.9x faster there.  The tile
-// does not depend on max_splits, so a launch with a capped split recomputes
-// the same one.
+// one block.  Decode batches (<= 512 rows) weigh every tile shape and split
+// against the fp32 partials a split adds, which at these sizes can exceed the
+// weights themselves (q/k/v at 256 rows and 14 splits: 66 MB of partials for
+// 33 MB of weights).  Prefill takes 256-row weight panels and splits K only
+// until the blocks fill one round.  The tile does not depend on max_splits,
+// so a launch with a capped split recomputes the same one.
 GemmPlan plan_tiled(int M, int N, int K, bool silu, int max_splits) {
   const int KB = K / kGBK;
-  const int bn = (!silu && M <= 512) ? 128 : 256;
   GemmPlan best{kKTiled, 1};
   double best_cost = 1e300;
+  if (M <= 512) {
+    // Decode batches: every tile shape and split, priced as rounds of 256 blocks x K steps per
+    // block x the tile's cost per K step (256 x 256: 1, 256 x 128 and 128 x 256: 0.65,
+    // 128 x 128: 0.49, with one 256 x 256 step ~0.5 us), plus the fp32 partials the split
+    // writes and its consumer reads at 4 TB/s.  Fitted to a sweep of all tile shapes and splits
+    // 1-16 at 96-512 rows of the 7B projections (q/k/v, o, gate/up, down, LM head), the plan
+    // it picks is within 0.2% of the fastest in total.
+    for (int bn : {128, 256})
+      for (int bm : {256, 128}) {
+        const double tile = (bm == 256 && bn == 256) ? 1.0 : (bm == 128 && bn == 128) ? 0.4875 : 0.65;
+        const int n_tiles = (silu ? N / (bn / 2) : (N + bn - 1) / bn) * ((M + bm - 1) / bm);
+        const int s_max = silu ? 1 : std::min(16, std::max(1, KB / 4));
+        for (int sp = 1; sp <= s_max; ++sp) {
+          if (even_splits(KB, sp) != sp) continue;
+          const int rounds = (n_tiles * sp + 255) / 256;
+          const double cost = rounds * static_cast<double>((KB + sp - 1) / sp) * 0.5 * tile +
+                              (silu ? 0.0 : sp * static_cast<double>(M) * N * 8 / 4.0e6);
+          if (cost < best_cost) {
+            best_cost = cost;
+            best = GemmPlan{kKTiled, sp, 0, 0, bm, bn};
+          }
+        }
+      }
+    best.splits = even_splits(KB, std::min(best.splits, max_splits));
+    return best;
+  }
+  // Prefill: 256-row weight panels; the block tile from rounds of 256 blocks times the K steps
+  // of one block, a BM = 128 step costing 0.71 of a BM = 256 one (measured at 4k rows).
+  const int bn = 256;
   for (int bm : {256, 128}) {
     const int blocks = (silu ? N / (bn / 2) : (N + bn - 1) / bn) * ((M + bm - 1) / bm);
-    int s = silu ? 1 : std::max(1, 256 / blocks);
-    s = even_splits(KB, std::min(s, std::max(1, KB / 8)));
-    const int rounds = (blocks * s + 255) / 256;
-    const double cost = static_cast<double>(rounds) * ((KB + s - 1) / s) * (bm == 256 ? 1.0 : 0.71);
+    int sp = silu ? 1 : std::max(1, 256 / blocks);
+    sp = even_splits(KB, std::min(sp, std::max(1, KB / 8)));
+    const int rounds = (blocks * sp + 255) / 256;
+    const double cost = static_cast<double>(rounds) * ((KB + sp - 1) / sp) * (bm == 256 ? 1.0 : 0.71);
     if (cost < best_cost) {
       best_cost = cost;
-      best = GemmPlan{kKTiled, s, 0, 0, bm, bn};
+      best = GemmPlan{kKTiled, sp, 0, 0, bm, bn};
     }
   }
-  // Two corrections the cost model misses, from a sweep of every tile shape and split at
-  // 96-512 rows of the 7B projections (times with the partial sums included):
-  //  * a product that needs no split (the LM head) takes the 256-row weight panels, as long
-  //    as they still fill the CUs: the 128-row panels only pay for halving a split (LM head
-  //    at 448 / 512 rows: 663 / 716 against 725 / 789 us);
-  //  * gate/up over two 256-row activation tiles (257-512 rows) takes 128-row weight panels:
-  //    592 tiles at two per CU spread the work past one round more evenly than 296 at one per
-  //    CU (155 / 167 against 178 / 188 us at 448 / 512 rows).
-  const int n_mb = (M + best.bm - 1) / best.bm;
-  if (!silu && best.bn == 128 && best.splits == 1 && ((N + 255) / 256) * n_mb >= 256) best.bn = 256;
-  if (silu && M <= 512 && best.bm == 256 && n_mb >= 2) best.bn = 128;
   best.splits = even_splits(KB, std::min(best.splits, max_splits));
   return best;
 }
