@@ -148,17 +148,20 @@ def test_bf16_decode_batch_shapes(model, layers, vocab, batches):
         assert r.max_rel_err <= 2e-2 and r.id_mismatch == 0, (B, r)
 
 
-def test_bf16_large_decode_batches():
-    """Decode batches above 64 rows run the LDS-tiled MFMA GEMM: 100 and 300 live rows take
-    128-row block tiles (the q/k/v, o and down products K-split), 200 rows 256-row tiles.  Every
-    row runs on the GPU; three per batch (first, middle, last: the ragged last block tile) are
-    compared with the oracle at the 7B layer shape."""
-    base = truncated(SHAPES["qwen2.5-7b"], 1, vocab=8192)
+@pytest.mark.parametrize("model,batches", [("qwen2.5-7b", (100, 200, 300)), ("qwen2.5-32b", (160, 300))])
+def test_bf16_large_decode_batches(model, batches):
+    """Decode batches above 64 rows run the LDS-tiled MFMA GEMM, whose plan picks a block tile
+    (128 or 256 activation rows x 128 or 256 weight rows) and a K split per product: at the 7B
+    layer 100 and 300 rows take 128-row activation tiles, 200 rows 256-row ones; the 32B layer
+    at 160 and 300 rows takes yet other pairs (256 x 128 q/k/v split 4, 256 x 256 down split 12,
+    128 x 256 q/k/v and o).  Every row runs on the GPU; three per batch (first, middle, last: the
+    ragged last block tile) are compared with the oracle."""
+    base = truncated(SHAPES[model], 1, vocab=8192)
     wd = make_weights(base, seed=2, device=DEV)
     w64 = weights_to_numpy(wd)
     rng = np.random.default_rng(6)
     from workloads.gen import Workload
-    for B in (100, 200, 300):
+    for B in batches:
         plen = rng.integers(1, 24, size=B)
         prompts = [rng.integers(0, base.vocab, size=int(p)).astype(np.int32) for p in plen]
         offs = np.zeros(B + 1, np.int64)
@@ -166,7 +169,7 @@ def test_bf16_large_decode_batches():
         wl = Workload("batch", base, np.arange(1000, 1000 + B, dtype=np.int64), np.concatenate(prompts), offs,
                       np.full(B, 3, np.int32), np.arange(B, dtype=np.int32), 1.0, 78)
         eng = _engine(base, wd, 320, 8192, 64, 2 * 320)
-        log(f"7b layer: decode batch B={B}")
+        log(f"{model} layer: decode batch B={B}")
         r = teacher_forced_parity(eng, base, w64, wl, 3, 2e-2, 1.0, 78, check=[0, B // 2, B - 1])
         eng.close()
         log(f"B={B}: {r}")
