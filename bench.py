@@ -17,8 +17,9 @@ Default workload: Qwen2.5-7B shape, bf16 random weights, the long round of 64
 sequences with long-tail forced response lengths (lognormal, median 4096,
 sigma 1.0, clamped to [512, 16384]), temperature 1.0.
 
-Prints one JSON line.  `--gpus N` with N > 1 is refused: this build runs on
-a single GPU.
+Prints one JSON line.  `--gpus N` with N > 1 is refused: the benchmark
+measures one GPU (data-parallel replicas are independent engines, one process
+per GPU, each with its own share of the sequences).
 """
 from __future__ import annotations
 
@@ -302,7 +303,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "rollout sequences shard across GPUs as independent engines, which this build does not run.",
+              "data-parallel replicas are independent engines, one process per GPU, and are not run here.",
               file=sys.stderr)
         sys.exit(2)
     t_start = time.perf_counter()
