@@ -10,8 +10,8 @@ record bench.py reads (kernel, workload, SHA-256 of the deep kernel's source
 text and launch plan, bytes per launch) and prints a table for the profile summary.  From the repository
 root:
 
-    python3 paper_2509_21009_amd/counter_traffic.py --pmc-dir gpurun_out \\
-        --stats gpurun_out/bench_kernel_stats.csv --out profiles/gate_up_traffic.json
+    python3 paper_2509_21009_amd/counter_traffic.py --pmc-dir results/pmc \\
+        --stats results/bench_kernel_stats.csv --out profiles/gate_up_traffic.json
 """
 from __future__ import annotations
 

@@ -20,8 +20,8 @@ and generated tokens) on the survivor with the fewest running requests; the
 projected length of a running request is the mean of the historical lengths
 above what it has already generated.
 
-    python3 paper_2509_21009_amd/replica_sim.py --trace gpurun_out/step_trace_7b.json
-    python3 paper_2509_21009_amd/replica_sim.py --model 3.7303,0.034094,5.2868e-6 --prefill-model 0,0.014164,0
+    python3 paper_2509_21009_amd/replica_sim.py --trace results/step_trace_7b.json
+    python3 paper_2509_21009_amd/replica_sim.py --model 3.5135,0.018858,5.9101e-6 --prefill-model 0,0.013172,0
 """
 from __future__ import annotations
 
